@@ -1,0 +1,330 @@
+"""Benchmark of the streaming action-decode step on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu] [--no-others]
+
+One "step" is one fv_decode_step (Algorithm 1, steady streaming): the full
+velocity pass of the action expert over the K-chunk buffer, the Euler update,
+emission, shift and noise refill, with inputs resident in HBM and the buffer
+carried over from step to step.  W untimed steps, then K timed steps between
+two device synchronisations; per-step latencies come from HIP events on the
+stream the library launches on.  Prints one JSON line.
+
+The headline workload is the pi0.5-shaped expert at batch 1 (18 layers,
+width 1024, 8q/1kv heads of 256, GeGLU 4096, prefix 560 = 2 views x 256 + 48
+text tokens, K = 10 chunks of 50 x 32 actions).  The other workloads (short
+chunks, batch 64 with ragged prefixes, the sequential 10-pass baseline) are
+measured in the same run and reported under "other_workloads".
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFS = 2500.0     # dense bf16 MFMA, TFLOP/s
+MFMA_FP32_PEAK_TFS = 157.3
+
+
+# ---------------------------------------------------------------- accounting
+
+def weight_bytes(w) -> int:
+    """Bytes of every weight one step reads once, at storage precision."""
+    e = 2 if w.dtype == synth.BF16 else 4
+    W, L, F, A = w.width, w.n_layers, w.mlp_dim, w.action_dim
+    qd, kd = w.n_q_heads * w.head_dim, w.n_kv_heads * w.head_dim
+    ngu = 2 * F if w.mlp_gated else F
+    mats = 2 * W * W + (6 * L + 2) * W * W
+    mats += L * (W * (qd + 2 * kd) + qd * W + W * ngu + F * W)
+    biases_f32 = 2 * W + (6 * L + 2) * W + W + A + A * W + W * A
+    return mats * e + biases_f32 * 4
+
+
+def step_bytes(w, lens) -> int:
+    e = 2 if w.dtype == synth.BF16 else 4
+    kv = 2 * int(np.sum(lens)) * w.n_kv_heads * w.head_dim * w.n_layers * e
+    buf = w.batch * w.tokens * w.action_dim * 4
+    io = 2 * buf + w.batch * w.chunk_len * w.action_dim * 4 + w.batch * w.n_chunks * 4
+    return weight_bytes(w) + kv + io
+
+
+def visible_pairs(w, P) -> int:
+    """Query-key pairs one stream's query token sees, summed over tokens (per head)."""
+    K, C = w.n_chunks, w.chunk_len
+    return w.tokens * int(P) + C * C * K * (K + 1) // 2
+
+
+def step_flops(w, lens):
+    """(GEMM flops, attention flops) of one velocity pass over real rows."""
+    W, L, F, A = w.width, w.n_layers, w.mlp_dim, w.action_dim
+    qd, kd = w.n_q_heads * w.head_dim, w.n_kv_heads * w.head_dim
+    ngu = 2 * F if w.mlp_gated else F
+    rows_t, rows_k = w.batch * w.tokens, w.batch * w.n_chunks
+    gemm = 2 * rows_k * W * W * 2 + 2 * rows_k * W * (6 * L + 2) * W
+    gemm += 2 * rows_t * A * W * 2
+    gemm += L * 2 * rows_t * (W * (qd + 2 * kd) + qd * W + W * ngu + F * W)
+    attn = sum(4 * w.head_dim * w.n_q_heads * visible_pairs(w, p) * L for p in lens)
+    return gemm, attn
+
+
+# ---------------------------------------------------------------- GPU side
+
+class Inputs:
+    def __init__(self, w, seed=0):
+        import torch
+        self.w = w
+        self.W = synth.make_weights(w, seed)
+        k, v, self.lens = synth.make_prefix(w, seed)
+        if w.dtype == synth.BF16:
+            self.kd = torch.from_numpy(synth.bf16_bits(k).view(np.int16)).cuda()
+            self.vd = torch.from_numpy(synth.bf16_bits(v).view(np.int16)).cuda()
+        else:
+            self.kd, self.vd = torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda()
+        self.host_k, self.host_v = k, v
+        self.x = synth.make_buffer(w, seed)
+        self.t = synth.noise_levels_batched(w)
+
+
+def _events(n):
+    import torch
+    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+
+
+def time_steps(fn, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    st, en = _events(steps), _events(steps)
+    t0 = time.perf_counter()
+    for i in range(steps):
+        st[i].record()
+        fn()
+        en[i].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [s.elapsed_time(e) for s, e in zip(st, en)]   # ms
+    total_ms = st[0].elapsed_time(en[-1])
+    return per, total_ms, wall
+
+
+def time_stage(ex, stage, layer, reps=200):
+    """Average duration (ms) of one launch of a stage, HIP events on its stream."""
+    import torch
+    ex.debug_stage(stage, layer, 10)
+    torch.cuda.synchronize()
+    s, e = _events(2)
+    s.record()
+    ex.debug_stage(stage, layer, reps)
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / reps
+
+
+def pct(xs, q):
+    return float(np.percentile(np.asarray(xs), q))
+
+
+def measure_streaming(w, steps, warmup, with_roofline):
+    import torch
+    from paper_2608_27384_amd.flashvla import Expert
+    inp = Inputs(w)
+    ex = Expert(inp.W, w, w.batch, w.max_prefix, noise_seed=w.noise_seed)
+    try:
+        ex.set_prefix(inp.kd, inp.vd, inp.lens)
+        xd = torch.from_numpy(inp.x).cuda()
+        td = torch.from_numpy(inp.t).cuda()
+        out = torch.empty((w.batch, w.chunk_len, w.action_dim), dtype=torch.float32,
+                          device="cuda")
+        per, total_ms, wall = time_steps(lambda: ex.decode_step(xd, td, out), steps, warmup)
+        assert bool(torch.isfinite(out).all()) and bool(torch.isfinite(xd).all()), \
+            "non-finite decode output"
+        ms = total_ms / steps
+        gemm_f, attn_f = step_flops(w, inp.lens)
+        nbytes = step_bytes(w, inp.lens)
+        res = {
+            "workload": w.name, "batch": w.batch, "n_chunks": w.n_chunks,
+            "chunk_len": w.chunk_len, "action_dim": w.action_dim,
+            "prefix_len": [int(inp.lens.min()), int(inp.lens.max())],
+            "steps": steps, "warmup": warmup, "ms_per_step": ms,
+            "chunks_per_s": w.batch / (ms / 1e3),
+            "p50_us": pct(per, 50) * 1e3, "p90_us": pct(per, 90) * 1e3,
+            "p99_us": pct(per, 99) * 1e3, "wall_s": wall,
+            "alg_bytes": nbytes, "alg_flops": gemm_f + attn_f,
+            "hbm_frac_step": nbytes / (ms / 1e3) / (HBM_PEAK_GBS * 1e9),
+            "mfma_frac_step": (gemm_f + attn_f) / (ms / 1e3) / (MFMA_BF16_PEAK_TFS * 1e12),
+        }
+        if with_roofline:
+            res["stages"] = stage_rooflines(ex, w, inp.lens)
+        return res
+    finally:
+        ex.close()
+
+
+def stage_rooflines(ex, w, lens):
+    """Per-launch algorithmic work and live-timed duration of the big stages."""
+    e = 2 if w.dtype == synth.BF16 else 4
+    W, F = w.width, w.mlp_dim
+    qd, kd = w.n_q_heads * w.head_dim, w.n_kv_heads * w.head_dim
+    ngu = 2 * F if w.mlp_gated else F
+    rows_t, rows_k = w.batch * w.tokens, w.batch * w.n_chunks
+    nmod = (6 * w.n_layers + 2) * W
+    peak = MFMA_BF16_PEAK_TFS if w.dtype == synth.BF16 else MFMA_FP32_PEAK_TFS
+    out = {}
+    specs = {
+        "film_maps": (0, 2 * rows_k * W * nmod, nmod * W * e + nmod * 4),
+        "qkv_gemm": (1, 2 * rows_t * W * (qd + 2 * kd), W * (qd + 2 * kd) * e),
+        "attention": (2, sum(4 * w.head_dim * w.n_q_heads * visible_pairs(w, p) for p in lens),
+                      2 * int(np.sum(lens)) * kd * e),
+        "gate_up_gemm": (3, 2 * rows_t * W * ngu, W * ngu * e),
+    }
+    for name, (stage, flops, nbytes) in specs.items():
+        ms = time_stage(ex, stage, 0)
+        out[name] = {"us": ms * 1e3, "tflops": flops / (ms / 1e3) / 1e12,
+                     "gbs": nbytes / (ms / 1e3) / 1e9,
+                     "mfma_frac": flops / (ms / 1e3) / (peak * 1e12),
+                     "hbm_frac": nbytes / (ms / 1e3) / (HBM_PEAK_GBS * 1e9),
+                     "flops": flops, "bytes": nbytes}
+    return out
+
+
+def measure_sequential(w, chunks, warmup):
+    import torch
+    from paper_2608_27384_amd.flashvla import Expert
+    inp = Inputs(w)
+    ex = Expert(inp.W, w, w.batch, w.max_prefix)
+    try:
+        ex.set_prefix(inp.kd, inp.vd, inp.lens)
+        noise = torch.from_numpy(np.ascontiguousarray(inp.x[:, 0])).cuda()
+        out = torch.empty_like(noise)
+        per, total_ms, wall = time_steps(lambda: ex.sequential_decode(noise, w.seq_steps, out),
+                                         chunks, warmup)
+        ms = total_ms / chunks
+        gemm_f, attn_f = step_flops(w, inp.lens)
+        nbytes = w.seq_steps * step_bytes(w, inp.lens)
+        return {"workload": w.name, "batch": w.batch, "passes_per_chunk": w.seq_steps,
+                "chunks": chunks, "ms_per_chunk": ms, "chunks_per_s": w.batch / (ms / 1e3),
+                "p50_us": pct(per, 50) * 1e3, "p99_us": pct(per, 99) * 1e3,
+                "alg_bytes": nbytes, "alg_flops": w.seq_steps * (gemm_f + attn_f),
+                "hbm_frac_step": nbytes / (ms / 1e3) / (HBM_PEAK_GBS * 1e9)}
+    finally:
+        ex.close()
+
+
+# ---------------------------------------------------------------- CPU side
+
+def cpu_baseline(w, budget_s=20.0):
+    """The CPU oracle (fp64) timed on this host on a bounded sample: decode
+    steps of the same workload, repeated until about budget_s has passed."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    W = synth.make_weights(w)
+    k, v, lens = synth.make_prefix(w)
+    x = synth.make_buffer(w)
+    t = synth.noise_levels_batched(w)
+    n, t0 = 0, time.perf_counter()
+    while True:
+        x, _ = oracle.decode_step(x, t, k, v, lens, W, w, noise_seed=0, step=n)
+        n += 1
+        el = time.perf_counter() - t0
+        if el > budget_s or n >= 50:
+            break
+    sec = el / n
+    return {"value": w.batch / sec, "unit": "chunks/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} fp64 oracle decode steps of {w.name} (batch {w.batch}), "
+                      f"{sec:.2f} s/step",
+            "s_per_step": sec}
+
+
+# ---------------------------------------------------------------- main
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="pi05_b1")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-others", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the decode step runs on a single MI355X and "
+              "independent streams shard without any exchange; run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+
+    w = synth.workload(args.workload)
+    main_res = measure_streaming(w, args.steps, args.warmup, with_roofline=True)
+    print(f"# {w.name}: {main_res['ms_per_step'] * 1e3:.1f} us/step, "
+          f"p50 {main_res['p50_us']:.1f} us", file=sys.stderr, flush=True)
+
+    others = {}
+    if not args.no_others:
+        for name, steps in (("short_chunk", 1000), ("batched64", 200)):
+            if name != w.name:
+                others[name] = measure_streaming(synth.workload(name), steps, 10, False)
+                print(f"# {name}: {others[name]['ms_per_step'] * 1e3:.1f} us/step",
+                      file=sys.stderr, flush=True)
+        others["seq_baseline"] = measure_sequential(synth.workload("seq_baseline"), 100, 10)
+        print(f"# seq_baseline: {others['seq_baseline']['ms_per_chunk'] * 1e3:.1f} us/chunk",
+              file=sys.stderr, flush=True)
+
+    stages = main_res.pop("stages")
+    dom_name = max(stages, key=lambda k: stages[k]["us"] * (
+        2 * w.n_layers if k not in ("film_maps",) else 1))
+    dom = stages[dom_name]
+    bound = "mfma" if dom["mfma_frac"] >= dom["hbm_frac"] else "hbm"
+    peak = MFMA_BF16_PEAK_TFS if w.dtype == synth.BF16 else MFMA_FP32_PEAK_TFS
+    roofline = {"kernel": dom_name, "bound": bound,
+                "achieved": dom["tflops"] if bound == "mfma" else dom["gbs"],
+                "peak": peak if bound == "mfma" else HBM_PEAK_GBS,
+                "unit": "TFLOP/s" if bound == "mfma" else "GB/s",
+                "frac": dom["mfma_frac"] if bound == "mfma" else dom["hbm_frac"],
+                "traffic": None, "us_per_launch": dom["us"]}
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(w)
+        print(f"# cpu oracle: {cpu['sample']}", file=sys.stderr, flush=True)
+
+    line = {
+        "metric": "action chunks/s (streaming decode step, pi0.5-shaped)",
+        "value": main_res["chunks_per_s"], "unit": "chunks/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": main_res["ms_per_step"],
+        "p50_us": main_res["p50_us"], "p90_us": main_res["p90_us"], "p99_us": main_res["p99_us"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == synth.BF16 else "fp32", "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "n_chunks": w.n_chunks,
+                   "chunk_len": w.chunk_len, "action_dim": w.action_dim,
+                   "prefix_len": main_res["prefix_len"], "layers": w.n_layers,
+                   "width": w.width, "parallelism": "single-gpu"},
+        "step_roofline": {"alg_bytes": main_res["alg_bytes"], "alg_flops": main_res["alg_flops"],
+                          "hbm_frac": main_res["hbm_frac_step"],
+                          "mfma_frac": main_res["mfma_frac_step"]},
+        "roofline": roofline,
+        "stages": stages,
+        "cpu_baseline": cpu,
+        "other_workloads": others,
+    }
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,350 @@
+// Chunk-wise causal attention of action tokens over [prefix ; buffer].
+//
+// The mask of the paper (Sec. 3.1: a noisier, later chunk attends to the
+// cleaner, earlier chunks, never the reverse, at chunk granularity; every
+// action token sees the cached observation) becomes a plain length limit
+// here: the QKV epilogue writes buffer token j of stream b at arena row
+// P_b + j, right after the P_b valid prefix rows, so a query of chunk k sees
+// exactly the key rows [0, P_b + C (k + 1)).  Rows beyond a query's limit are
+// scored -inf, giving probability exactly 0.
+//
+// Work split: the query rows of one (stream, kv head) are the (token, head)
+// pairs of its query-head group, flattened token-major; a block of 4 waves
+// takes 128 consecutive rows (32 per wave, as two 16-row MFMA groups that
+// share every K and V fragment read from LDS), so rows of all heads that
+// share the kv head reuse one K/V tile.  The next K/V tile is loaded into
+// registers while the current one is multiplied.  Rows of a block may straddle a chunk
+// boundary; each lane masks with its own row's limit.  Optionally the key
+// tiles of a block are split over gridDim.z blocks whose partial (o, max,
+// sum) are merged in a fixed order by attn_combine.
+//
+// Per key tile (KT keys): K [KT][dh] and V^T [dh][KT] are staged in LDS;
+// each wave forms S^T = K Q^T with MFMA, so a lane holds the scores of one
+// query for 4 keys per 16-key subtile; the row max and row sum need only two
+// cross-lane exchanges (lanes l, l^16, l^32, l^48); the probabilities are
+// then, without any data movement, the B operand of O^T += V^T P^T.
+#include "fv_internal.h"
+
+namespace fv {
+
+namespace {
+
+constexpr int kRowsPerWave = 32;                 // two 16-row MFMA groups
+constexpr float kSlack = 8.0f;                   // lazy softmax reference slack (log2)
+constexpr int kRowsPerBlock = 4 * kRowsPerWave;
+
+template <typename T, int DH, int KT>
+__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
+  using MF = Mfma<T>;
+  constexpr int EPV = 16 / (int)sizeof(T);
+  constexpr int LDK = DH + EPV;
+  constexpr int LDV = KT + EPV;
+  constexpr int NST = KT / 16;
+  constexpr int NKS = DH / MF::KM;
+  constexpr int NDT = DH / 16;
+  constexpr int VK = KT * DH / EPV, VV = DH * KT / EPV;  // 16-byte vectors per tile
+  constexpr int NVK = (VK + 255) / 256, NVV = (VV + 255) / 256;
+  constexpr bool kBF16 = sizeof(T) == 2;
+  static_assert(!kBF16 || NST % 2 == 0, "bf16 path pairs 16-key subtiles");
+
+  __shared__ __attribute__((aligned(16))) T sK[KT * LDK];
+  __shared__ __attribute__((aligned(16))) T sV[DH * LDV];
+
+  const int G = a.n_q_heads / a.n_kv_heads;
+  const int rows_bg = a.tokens * G;
+  const int tile0 = blockIdx.x * kRowsPerBlock;
+  const int b = blockIdx.y / a.n_kv_heads, g = blockIdx.y - b * a.n_kv_heads;
+  const int split = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int P = a.len[b];
+  const int C = a.chunk_len;
+  const int l16 = lane & 15, lg = lane >> 4;
+
+  // this lane's two query rows (one per 16-row group)
+  int tok[2], head[2], lim[2];
+  bool valid[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int rq = tile0 + kRowsPerWave * wave + 16 * q + l16;
+    valid[q] = rq < rows_bg;
+    const int rqc = valid[q] ? rq : rows_bg - 1;
+    tok[q] = rqc / G;
+    head[q] = g * G + (rqc - tok[q] * G);
+    lim[q] = P + C * (tok[q] / C + 1);
+  }
+  const int rlast = min(tile0 + kRowsPerBlock - 1, rows_bg - 1);
+  const int lim_max = P + C * ((rlast / G) / C + 1);
+  const int nkt = (lim_max + KT - 1) / KT;
+  const int kt_begin = (split * nkt) / a.n_split, kt_end = ((split + 1) * nkt) / a.n_split;
+
+  typename MF::frag qf[2][NKS];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const T* qrow = reinterpret_cast<const T*>(a.q) +
+                    ((size_t)(b * a.tokens + tok[q]) * a.n_q_heads + head[q]) * DH;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qf[q][ks] = MF::load(qrow + ks * MF::KM + MF::KG * lg);
+  }
+
+  f32x4 acc[2][NDT];
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) acc[q][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+
+  const T* kbase = reinterpret_cast<const T*>(a.karena) +
+                   ((size_t)b * a.n_kv_heads + g) * (size_t)a.S * DH;
+  const T* vbase = reinterpret_cast<const T*>(a.vtarena) +
+                   ((size_t)b * a.n_kv_heads + g) * (size_t)DH * a.S;
+  const float sl2 = 1.4426950408889634f / sqrtf((float)DH);
+
+  // register stage of one K / V^T tile (loads issued unconditionally; a
+  // clamped tile index keeps the addresses in bounds)
+  u32x4 rk[NVK], rv[NVV];
+  auto load_tile = [&](int kt) __attribute__((always_inline)) {
+    const int key0 = kt * KT;
+#pragma unroll
+    for (int i = 0; i < NVK; ++i) {
+      const int vi = tid + 256 * i;
+      if (VK % 256 == 0 || vi < VK) {
+        const int r = vi / (DH / EPV), c = vi - r * (DH / EPV);
+        rk[i] = *reinterpret_cast<const u32x4*>(kbase + (size_t)(key0 + r) * DH + c * EPV);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NVV; ++i) {
+      const int vi = tid + 256 * i;
+      if (VV % 256 == 0 || vi < VV) {
+        const int r = vi / (KT / EPV), c = vi - r * (KT / EPV);
+        rv[i] = *reinterpret_cast<const u32x4*>(vbase + (size_t)r * a.S + key0 + c * EPV);
+      }
+    }
+  };
+  auto store_tile = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < NVK; ++i) {
+      const int vi = tid + 256 * i;
+      if (VK % 256 == 0 || vi < VK) {
+        const int r = vi / (DH / EPV), c = vi - r * (DH / EPV);
+        *reinterpret_cast<u32x4*>(&sK[r * LDK + c * EPV]) = rk[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NVV; ++i) {
+      const int vi = tid + 256 * i;
+      if (VV % 256 == 0 || vi < VV) {
+        const int r = vi / (KT / EPV), c = vi - r * (KT / EPV);
+        *reinterpret_cast<u32x4*>(&sV[r * LDV + c * EPV]) = rv[i];
+      }
+    }
+  };
+
+  const int kt_clamp = max(kt_begin, kt_end - 1);
+  load_tile(min(kt_begin, kt_clamp));
+  for (int kt = kt_begin; kt < kt_end; ++kt) {
+    const int key0 = kt * KT;
+    __syncthreads();  // previous tile fully consumed
+    store_tile();
+    __syncthreads();
+    load_tile(min(kt + 1, kt_clamp));  // overlaps the MFMA work below
+
+    // S^T = K Q^T for both row groups; K fragments are shared
+    f32x4 s[2][NST];
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+      s[0][st] = f32x4{0.f, 0.f, 0.f, 0.f};
+      s[1][st] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        const typename MF::frag kf =
+            MF::load(&sK[(16 * st + l16) * LDK + ks * MF::KM + MF::KG * lg]);
+        s[0][st] = MF::mma(kf, qf[0][ks], s[0][st]);
+        s[1][st] = MF::mma(kf, qf[1][ks], s[1][st]);
+      }
+    }
+    // Online softmax per query row (a lane owns one row of each group) with
+    // a lazily moved reference: exponents are taken against m_run, which
+    // only moves when a row's tile maximum exceeds it by more than kSlack
+    // (log2 units), so probabilities stay below 2^kSlack and the costly
+    // rescale of the accumulators runs only when some row of the wave moved.
+    bool moved = false;
+    float alpha[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      float mt = -INFINITY;
+#pragma unroll
+      for (int st = 0; st < NST; ++st)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = key0 + 16 * st + 4 * lg + r;
+          const float x = key < lim[q] ? s[q][st][r] * sl2 : -INFINITY;
+          s[q][st][r] = x;
+          mt = fmaxf(mt, x);
+        }
+      mt = fmaxf(mt, __shfl_xor(mt, 16));
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      const float m_new = mt > m_run[q] + kSlack ? mt : m_run[q];
+      alpha[q] = 1.f;
+      if (m_new != m_run[q]) {
+        // acc and l are still zero while m_run is -inf
+        alpha[q] = m_run[q] == -INFINITY ? 0.f : exp2f(m_run[q] - m_new);
+        moved = true;
+      }
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      float ls = 0.f;
+#pragma unroll
+      for (int st = 0; st < NST; ++st)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = exp2f(s[q][st][r] - m_use);
+          s[q][st][r] = p;
+          ls += p;
+        }
+      ls += __shfl_xor(ls, 16);
+      ls += __shfl_xor(ls, 32);
+      l_run[q] = l_run[q] * alpha[q] + ls;
+      m_run[q] = m_new;
+    }
+    if (__builtin_amdgcn_read_exec() && __any(moved)) {
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) acc[q][dt] *= alpha[q];
+    }
+
+    // O^T += V^T P^T; V^T fragments are shared by both row groups
+    if constexpr (kBF16) {
+#pragma unroll
+      for (int kc = 0; kc < NST / 2; ++kc) {
+        bf16x8 pf[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          u16x8 pb;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            pb[r] = f32_to_bf16(s[q][2 * kc][r]);
+            pb[4 + r] = f32_to_bf16(s[q][2 * kc + 1][r]);
+          }
+          pf[q] = __builtin_bit_cast(bf16x8, pb);
+        }
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          const T* vr = &sV[(16 * dt + l16) * LDV + 32 * kc + 4 * lg];
+          const u16x4 lo = *reinterpret_cast<const u16x4*>(vr);
+          const u16x4 hi = *reinterpret_cast<const u16x4*>(vr + 16);
+          const bf16x8 vf = __builtin_bit_cast(
+              bf16x8, u16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+          acc[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[0], acc[0][dt], 0, 0, 0);
+          acc[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[1], acc[1][dt], 0, 0, 0);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int st = 0; st < NST; ++st)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int dt = 0; dt < NDT; ++dt) {
+            const float vf = (float)sV[(16 * dt + l16) * LDV + 16 * st + 4 * lg + r];
+            acc[0][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, (float)s[0][st][r], acc[0][dt],
+                                                              0, 0, 0);
+            acc[1][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, (float)s[1][st][r], acc[1][dt],
+                                                              0, 0, 0);
+          }
+    }
+  }
+
+  const size_t R = (size_t)a.B * a.tokens * a.n_q_heads;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    if (!valid[q]) continue;
+    const size_t grow = (size_t)(b * a.tokens + tok[q]) * a.n_q_heads + head[q];
+    if (a.n_split == 1) {
+      const float inv = 1.0f / l_run[q];
+      T* orow = reinterpret_cast<T*>(a.o) + grow * DH;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) orow[16 * dt + 4 * lg + r] = from_f32<T>(acc[q][dt][r] * inv);
+    } else {
+      float* po = a.part_o + ((size_t)split * R + grow) * DH;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) *reinterpret_cast<f32x4*>(po + 16 * dt + 4 * lg) = acc[q][dt];
+      if (lg == 0) {
+        a.part_ml[((size_t)split * R + grow) * 2 + 0] = m_run[q];
+        a.part_ml[((size_t)split * R + grow) * 2 + 1] = l_run[q];
+      }
+    }
+  }
+}
+
+// Merge of split partials in split order: o = sum_z 2^(m_z - M) o_z / sum_z 2^(m_z - M) l_z.
+// One wave per row; a lane owns 4 consecutive features.
+template <typename T, int DH>
+__global__ __launch_bounds__(256) void attn_combine(const float* __restrict__ part_o,
+                                                    const float* __restrict__ part_ml,
+                                                    T* __restrict__ o, int R, int n_split) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= R) return;
+  float M = -INFINITY;
+  float mz[8], lz[8];
+  for (int z = 0; z < n_split; ++z) {
+    mz[z] = part_ml[((size_t)z * R + row) * 2];
+    lz[z] = part_ml[((size_t)z * R + row) * 2 + 1];
+    M = fmaxf(M, mz[z]);
+  }
+  float den = 0.f;
+  for (int z = 0; z < n_split; ++z) {
+    mz[z] = exp2f(mz[z] - M);
+    den += mz[z] * lz[z];
+  }
+  const float inv = 1.0f / den;
+  for (int d = 4 * lane; d < DH; d += 256) {
+    f32x4 num = {0.f, 0.f, 0.f, 0.f};
+    for (int z = 0; z < n_split; ++z)
+      num += mz[z] * *reinterpret_cast<const f32x4*>(part_o + ((size_t)z * R + row) * DH + d);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[(size_t)row * DH + d + i] = from_f32<T>(num[i] * inv);
+  }
+}
+
+template <typename T, int DH>
+void launch_dh(const AttnArgs& a, hipStream_t s) {
+  // 32-key tiles keep wide heads (and fp32) within the register file
+  constexpr int KT = (sizeof(T) == 2 && DH < 192) ? 64 : 32;
+  const int G = a.n_q_heads / a.n_kv_heads;
+  dim3 grid((a.tokens * G + kRowsPerBlock - 1) / kRowsPerBlock, a.B * a.n_kv_heads, a.n_split);
+  hipLaunchKernelGGL((attn_kernel<T, DH, KT>), grid, dim3(256), 0, s, a);
+  if (a.n_split > 1) {
+    const int R = a.B * a.tokens * a.n_q_heads;
+    hipLaunchKernelGGL((attn_combine<T, DH>), dim3((R + 3) / 4), dim3(256), 0, s, a.part_o, a.part_ml,
+                       reinterpret_cast<T*>(a.o), R, a.n_split);
+  }
+}
+
+}  // namespace
+
+template <typename T>
+int attention_row_tiles(int tokens, int n_q_heads, int n_kv_heads) {
+  return (tokens * (n_q_heads / n_kv_heads) + kRowsPerBlock - 1) / kRowsPerBlock;
+}
+
+template <typename T>
+void launch_attention(const AttnArgs& a, hipStream_t s) {
+  switch (a.head_dim) {
+    case 64: launch_dh<T, 64>(a, s); break;
+    case 128: launch_dh<T, 128>(a, s); break;
+    case 192: launch_dh<T, 192>(a, s); break;
+    case 256: launch_dh<T, 256>(a, s); break;
+    default: break;  // rejected at fv_create
+  }
+}
+
+template void launch_attention<bf16_t>(const AttnArgs&, hipStream_t);
+template void launch_attention<float>(const AttnArgs&, hipStream_t);
+template int attention_row_tiles<bf16_t>(int, int, int);
+template int attention_row_tiles<float>(int, int, int);
+
+}  // namespace fv

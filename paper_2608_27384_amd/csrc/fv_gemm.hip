@@ -1,0 +1,544 @@
+// MFMA GEMMs of the action expert with fused epilogues.
+//
+// Every linear layer of the expert (time-MLP, FiLM maps, packed QKV, output
+// projection, packed gate/up, down projection) is C = A * W with A the
+// activations [M][K] (row-major) and W stored output-major as Bt [N][K].
+//
+// Block: NW waves (4 or 8).  Tile BM x BN; k is staged through LDS 128 bytes
+// per row (64 bf16 / 32 fp32) at a time in two buffers.  While a wave
+// multiplies the tile in one buffer with 32x32 MFMA instructions, the
+// registers holding the next tile are written to the other buffer piece by
+// piece between k-steps, and every freed register piece immediately issues
+// its global load of the tile after that, so MFMA work, LDS writes and global
+// loads overlap; one barrier per k-tile.  Rows of A beyond M re-read row M-1
+// (never stored).
+//
+// Split-K (KS > 1): block z of a tile accumulates k-tiles [z*nk/KS,
+// (z+1)*nk/KS) and writes its fp32 partial tile to a workspace; a second,
+// small kernel sums the KS partials of each tile in split order (so the
+// result does not depend on scheduling) and runs the epilogue.  The kernel
+// boundary makes the partials visible across the chip's separate L2 caches
+// without device-wide cache flushes inside the GEMM.
+//
+// Epilogues consume the accumulators in registers:
+//  * bias + SiLU (time-MLP), bias to fp32 (FiLM maps);
+//  * QKV: queries and keys are rotated (half-split rotary pairs) and keys and
+//    values are written straight into the layer's K / V^T arena at row
+//    len[b] + token, so attention reads [prefix ; buffer] as one key range;
+//  * gated residual h += gate[chunk] * acc;
+//  * GeGLU gelu(g) * u and plain GELU.
+// Paired epilogues rely on the weight packing: columns [64p, 64p+32) and
+// [64p+32, 64p+64) of a packed matrix hold the two partners of a pair, which
+// then sit in the same lane and register of two adjacent 32-column tiles.
+#include "fv_internal.h"
+
+namespace fv {
+
+namespace {
+
+// 32x32 MFMA per element type: bf16 32x32x16 (8 k per lane), fp32 32x32x2
+// (1 k per lane).  Output layout (both): lane l, register r holds
+// row 8*(r/4) + 4*(l/32) + r%4, column l%32 of the 32x32 tile.
+template <typename T> struct Mf32;
+template <> struct Mf32<bf16_t> {
+  static constexpr int KG = 8, KM = 16;
+  typedef bf16x8 frag;
+  __device__ static __forceinline__ frag load(const bf16_t* p) {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(p));
+  }
+  __device__ static __forceinline__ f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct Mf32<float> {
+  static constexpr int KG = 1, KM = 2;
+  typedef float frag;
+  __device__ static __forceinline__ frag load(const float* p) { return *p; }
+  __device__ static __forceinline__ f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+};
+
+__device__ __forceinline__ int acc_row(int r, int lane) {
+  return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+}
+
+template <typename T, int BM, int BN, int NW, int WGM, class Epi>
+__global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ A,
+                                                       const T* __restrict__ Bt, int M, int N,
+                                                       int K, int KS, float* __restrict__ ws,
+                                                       Epi epi) {
+  using MF = Mf32<T>;
+  constexpr int NT = 64 * NW;
+  constexpr int WGN = NW / WGM;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int FM = WTM / 32, FN = WTN / 32;
+  constexpr int EPV = 16 / (int)sizeof(T);  // elements per 16-byte vector
+  constexpr int BK = 8 * EPV;               // 128 bytes of k per row and stage
+  constexpr int LDR = BK + EPV;             // LDS row pitch (one vector of padding)
+  constexpr int VA = BM * 8, VB = BN * 8;   // 16-byte vectors per stage
+  constexpr int NA = (VA + NT - 1) / NT, NB = (VB + NT - 1) / NT;
+  constexpr int NSTEP = BK / MF::KM;
+  static_assert(FM >= 1 && FN >= 1 && WGM * WGN == NW, "bad tile");
+
+  __shared__ __attribute__((aligned(16))) T sA[2][BM * LDR];
+  __shared__ __attribute__((aligned(16))) T sB[2][BN * LDR];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WGM, wn = wave / WGM;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int arow = wm * WTM, brow = wn * WTN;
+  const int nk_all = K / BK;
+  const int kz = blockIdx.z;
+  const int kt0 = (kz * nk_all) / KS, kt1 = ((kz + 1) * nk_all) / KS;
+  const int klast = (kt1 - 1) * BK;
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
+
+  u32x4 ra[NA], rb[NB];
+#pragma unroll
+  for (int i = 0; i < NA; ++i) ra[i] = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int i = 0; i < NB; ++i) rb[i] = u32x4{0u, 0u, 0u, 0u};
+
+  // Prologue: tile kt0 into LDS[0], tile kt0+1 into registers.
+#pragma unroll
+  for (int step = 0; step < 2; ++step) {
+    const int k0 = step == 0 ? kt0 * BK : min((kt0 + 1) * BK, klast);
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int vi = tid + NT * i;
+      if (VA % NT == 0 || vi < VA) {
+        const int r = vi >> 3, c = vi & 7;
+        const int gr = min(m0 + r, M - 1);
+        ra[i] = *reinterpret_cast<const u32x4*>(A + (size_t)gr * K + k0 + c * EPV);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int vi = tid + NT * i;
+      if (VB % NT == 0 || vi < VB) {
+        const int r = vi >> 3, c = vi & 7;
+        rb[i] = *reinterpret_cast<const u32x4*>(Bt + (size_t)(n0 + r) * K + k0 + c * EPV);
+      }
+    }
+    if (step == 0) {
+#pragma unroll
+      for (int i = 0; i < NA; ++i) {
+        const int vi = tid + NT * i;
+        if (VA % NT == 0 || vi < VA)
+          *reinterpret_cast<u32x4*>(&sA[0][(vi >> 3) * LDR + (vi & 7) * EPV]) = ra[i];
+      }
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        const int vi = tid + NT * i;
+        if (VB % NT == 0 || vi < VB)
+          *reinterpret_cast<u32x4*>(&sB[0][(vi >> 3) * LDR + (vi & 7) * EPV]) = rb[i];
+      }
+    }
+  }
+  __syncthreads();
+
+  const int lr = lane & 31, lk = MF::KG * (lane >> 5);
+  for (int kt = kt0; kt < kt1; ++kt) {
+    const int cur = (kt - kt0) & 1;
+    const int knext = min((kt + 2) * BK, klast);  // unconditional prefetch (clamped)
+#pragma unroll
+    for (int ks = 0; ks < NSTEP; ++ks) {
+      typename MF::frag af[FM], bfr[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        af[i] = MF::load(&sA[cur][(arow + 32 * i + lr) * LDR + ks * MF::KM + lk]);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        bfr[j] = MF::load(&sB[cur][(brow + 32 * j + lr) * LDR + ks * MF::KM + lk]);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = MF::mma(af[i], bfr[j], acc[i][j]);
+      // register pieces of the next tile assigned to this k-step: store them
+      // into the other buffer, then reload them with the tile after that
+#pragma unroll
+      for (int i = 0; i < NA; ++i) {
+        if ((i * NSTEP) / NA != ks) continue;
+        const int vi = tid + NT * i;
+        if (VA % NT == 0 || vi < VA) {
+          const int r = vi >> 3, c = vi & 7;
+          *reinterpret_cast<u32x4*>(&sA[cur ^ 1][r * LDR + c * EPV]) = ra[i];
+          const int gr = min(m0 + r, M - 1);
+          ra[i] = *reinterpret_cast<const u32x4*>(A + (size_t)gr * K + knext + c * EPV);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        if ((i * NSTEP) / NB != ks) continue;
+        const int vi = tid + NT * i;
+        if (VB % NT == 0 || vi < VB) {
+          const int r = vi >> 3, c = vi & 7;
+          *reinterpret_cast<u32x4*>(&sB[cur ^ 1][r * LDR + c * EPV]) = rb[i];
+          rb[i] = *reinterpret_cast<const u32x4*>(Bt + (size_t)(n0 + r) * K + knext + c * EPV);
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  if (KS > 1) {
+    // Partial tile -> workspace, row-major [KS][M][N] fp32 (lanes of a row
+    // write 32 consecutive columns); summed in split order afterwards.
+    float* part = ws + (size_t)kz * M * N;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = n0 + brow + 32 * j + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + arow + 32 * i + acc_row(r, lane);
+          if (row < M) part[(size_t)row * N + col] = acc[i][j][r];
+        }
+      }
+    return;
+  }
+  epi.template apply<FM, FN>(acc, m0 + arow, n0 + brow, lane, M);
+}
+
+// Sum of the KS split partials of each tile, in split order, followed by the
+// epilogue; same block shape and register layout as the GEMM that wrote them.
+template <int BM, int BN, int NW, int WGM, class Epi>
+__global__ __launch_bounds__(64 * NW) void gemm_reduce_kernel(const float* __restrict__ ws, int M,
+                                                              int N, int KS, Epi epi) {
+  constexpr int WGN = NW / WGM;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int FM = WTM / 32, FN = WTN / 32;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave % WGM, wn = wave / WGM;
+  const int row0 = blockIdx.y * BM + wm * WTM, col0 = blockIdx.x * BN + wn * WTN;
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
+  for (int z = 0; z < KS; ++z) {  // split order; loads within a split are independent
+    const float* part = ws + (size_t)z * M * N;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = col0 + 32 * j + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = min(row0 + 32 * i + acc_row(r, lane), M - 1);
+          acc[i][j][r] += part[(size_t)row * N + col];
+        }
+      }
+  }
+  epi.template apply<FM, FN>(acc, row0, col0, lane, M);
+}
+
+// ----------------------------------------------------------------- epilogues
+// Element (i, j, r) of a wave's accumulators sits at
+//   row = row0 + 32 i + acc_row(r, lane),   col = col0 + 32 j + lane % 32.
+
+template <typename T>
+struct EpiBiasSilu {
+  T* out; const float* bias; int ldo;
+  template <int FM, int FN>
+  __device__ void apply(f32x16 (&acc)[FM][FN], int row0, int col0, int lane, int M) const {
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int col = col0 + 32 * j + (lane & 31);
+      const float b = bias[col];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = row0 + 32 * i + acc_row(r, lane);
+          if (row < M) out[(size_t)row * ldo + col] = from_f32<T>(silu_f(acc[i][j][r] + b));
+        }
+    }
+  }
+};
+
+struct EpiBiasF32 {
+  float* out; const float* bias; int ldo;
+  template <int FM, int FN>
+  __device__ void apply(f32x16 (&acc)[FM][FN], int row0, int col0, int lane, int M) const {
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int col = col0 + 32 * j + (lane & 31);
+      const float b = bias[col];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = row0 + 32 * i + acc_row(r, lane);
+          if (row < M) out[(size_t)row * ldo + col] = acc[i][j][r] + b;
+        }
+    }
+  }
+};
+
+template <typename T>
+struct EpiQkv {
+  QkvArgs<T> a;
+  template <int FM, int FN>
+  __device__ void apply(f32x16 (&acc)[FM][FN], int row0, int col0, int lane, int M) const {
+    static_assert(FN % 2 == 0, "QKV epilogue needs column pairs");
+    const int dh = a.head_dim, half = dh / 2;
+    const int qd = a.n_q_heads * dh, kd = a.n_kv_heads * dh;
+#pragma unroll
+    for (int j = 0; j < FN; j += 2) {
+      const int c0 = col0 + 32 * j;  // first packed column of the pair group
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = row0 + 32 * i + acc_row(r, lane);
+          if (row >= M) continue;
+          const int2 rp = a.row_pos[row];  // (stream, arena row)
+          const int b = rp.x, pos = rp.y;
+          const float x0 = acc[i][j][r], x1 = acc[i][j + 1][r];
+          if (c0 < qd + kd) {
+            const bool isq = c0 < qd;
+            const int cc = isq ? c0 : c0 - qd;
+            const int head = cc / dh;
+            const int dlo = 32 * ((cc - head * dh) >> 6) + (lane & 31), dhi = dlo + half;
+            const float cs = a.rcos[(size_t)pos * half + dlo];
+            const float sn = a.rsin[(size_t)pos * half + dlo];
+            const float y0 = x0 * cs - x1 * sn, y1 = x1 * cs + x0 * sn;
+            T* dst = isq ? a.q + (size_t)row * qd + head * dh
+                         : a.karena + (((size_t)b * a.n_kv_heads + head) * a.S + pos) * dh;
+            dst[dlo] = from_f32<T>(y0);
+            dst[dhi] = from_f32<T>(y1);
+          } else {
+            const int cc = c0 - qd - kd;
+            const int g = cc / dh, d = cc - g * dh + (lane & 31);
+            T* base = a.vtarena + ((size_t)b * a.n_kv_heads + g) * dh * a.S + pos;
+            base[(size_t)d * a.S] = from_f32<T>(x0);
+            base[(size_t)(d + 32) * a.S] = from_f32<T>(x1);
+          }
+        }
+    }
+  }
+};
+
+struct EpiGatedResid {
+  float* h; const float* mod; int mod_ld, gate_off, chunk_len, ldh;
+  template <int FM, int FN>
+  __device__ void apply(f32x16 (&acc)[FM][FN], int row0, int col0, int lane, int M) const {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = row0 + 32 * i + acc_row(r, lane);
+        if (row >= M) continue;
+        const float* g = mod + (size_t)(row / chunk_len) * mod_ld + gate_off;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int col = col0 + 32 * j + (lane & 31);
+          float* hp = h + (size_t)row * ldh + col;
+          *hp = *hp + g[col] * acc[i][j][r];
+        }
+      }
+  }
+};
+
+template <typename T>
+struct EpiGeglu {
+  T* out; int ldo;
+  template <int FM, int FN>
+  __device__ void apply(f32x16 (&acc)[FM][FN], int row0, int col0, int lane, int M) const {
+    static_assert(FN % 2 == 0, "GeGLU epilogue needs column pairs");
+#pragma unroll
+    for (int j = 0; j < FN; j += 2) {
+      const int col = ((col0 + 32 * j) >> 1) + (lane & 31);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = row0 + 32 * i + acc_row(r, lane);
+          if (row < M)
+            out[(size_t)row * ldo + col] =
+                from_f32<T>(gelu_tanh_f(acc[i][j][r]) * acc[i][j + 1][r]);
+        }
+    }
+  }
+};
+
+template <typename T>
+struct EpiGelu {
+  T* out; int ldo;
+  template <int FM, int FN>
+  __device__ void apply(f32x16 (&acc)[FM][FN], int row0, int col0, int lane, int M) const {
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int col = col0 + 32 * j + (lane & 31);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = row0 + 32 * i + acc_row(r, lane);
+          if (row < M) out[(size_t)row * ldo + col] = from_f32<T>(gelu_tanh_f(acc[i][j][r]));
+        }
+    }
+  }
+};
+
+// -------------------------------------------------------------- tile choice
+// Tile shapes (BM x BN, waves); every wave owns a sub-tile at least 64
+// columns wide, so paired epilogues find both partners of a 64-column pair
+// group in one wave.
+enum Tile { T256x128w8 = 0, T128x128w8 = 1, T64x128w4 = 2, T32x128w2 = 3 };
+constexpr int kTileBM[] = {256, 128, 64, 32};
+constexpr int kTileBN[] = {128, 128, 128, 128};
+
+template <typename T, int BM, int BN, int NW, int WGM, class Epi>
+void launch_tile(const T* A, const T* Bt, int M, int N, int K, const GemmPlan& p,
+                 const GemmWork& w, const Epi& epi, hipStream_t s) {
+  dim3 grid(N / BN, (M + BM - 1) / BM, p.ks);
+  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, NW, WGM, Epi>), grid, dim3(64 * NW), 0, s, A, Bt, M,
+                     N, K, p.ks, w.ws, epi);
+  if (p.ks > 1)
+    hipLaunchKernelGGL((gemm_reduce_kernel<BM, BN, NW, WGM, Epi>), dim3(grid.x, grid.y),
+                       dim3(64 * NW), 0, s, w.ws, M, N, p.ks, epi);
+}
+
+template <typename T, class Epi>
+void run_gemm(const T* A, const T* Bt, int M, int N, int K, const GemmWork& w, const Epi& epi,
+              hipStream_t s) {
+  if (M <= 0) return;
+  const GemmPlan p = plan_gemm(M, N, K, sizeof(T) == 2);
+  switch (p.tile) {
+    case T256x128w8: launch_tile<T, 256, 128, 8, 4>(A, Bt, M, N, K, p, w, epi, s); break;
+    case T128x128w8: launch_tile<T, 128, 128, 8, 4>(A, Bt, M, N, K, p, w, epi, s); break;
+    case T64x128w4: launch_tile<T, 64, 128, 4, 2>(A, Bt, M, N, K, p, w, epi, s); break;
+    case T32x128w2: launch_tile<T, 32, 128, 2, 1>(A, Bt, M, N, K, p, w, epi, s); break;
+    default: break;  // N % 128 != 0 is rejected at fv_create
+  }
+}
+
+}  // namespace
+
+// Tile by row count: large M takes big tiles (fewer re-reads of A and W);
+// medium M takes 128x128 tiles when that still gives about 200 blocks, else
+// 64x128; small M takes 64- or 32-row tiles.  When fewer than 128 tiles
+// exist, k is split (KS a power of two, at least 4 k-tiles per split, at most
+// about 320 blocks) so that every CU streams its share of the weights.
+GemmPlan plan_gemm(int M, int N, int K, bool bf16) {
+  GemmPlan p;
+  if (N % 128 || M <= 0) return p;
+  const int bk = bf16 ? 64 : 32, nk = K / bk;
+  auto ntiles = [&](int t) { return ((M + kTileBM[t] - 1) / kTileBM[t]) * (N / kTileBN[t]); };
+  if (M >= 4096)
+    p.tile = T256x128w8;
+  else if (M > 256)
+    p.tile = ntiles(T128x128w8) >= 200 ? T128x128w8 : T64x128w4;
+  else if (M > 32)
+    p.tile = T64x128w4;
+  else
+    p.tile = T32x128w2;
+  const int bm = kTileBM[p.tile], bn = kTileBN[p.tile];
+  p.tiles = ntiles(p.tile);
+  p.ks = 1;
+  if (p.tiles < 128)
+    while ((long)p.tiles * p.ks * 2 <= 320 && nk / (p.ks * 2) >= 4 && p.ks < 8) p.ks *= 2;
+  p.ws_floats = p.ks > 1 ? (size_t)p.ks * M * N : 0;
+  (void)bm;
+  (void)bn;
+  return p;
+}
+
+// Raw split partials only (no epilogue); the caller reduces them.
+struct EpiNone {
+  template <int FM, int FN>
+  __device__ void apply(f32x16 (&)[FM][FN], int, int, int, int) const {}
+};
+
+template <typename T>
+int gemm_partials(const T* A, const T* Bt, int M, int N, int K, const GemmWork& w,
+                  hipStream_t s) {
+  const GemmPlan p = plan_gemm(M, N, K, sizeof(T) == 2);
+  if (p.ks <= 1) return 1;
+  switch (p.tile) {
+    case T256x128w8: {
+      dim3 g(N / 128, (M + 255) / 256, p.ks);
+      hipLaunchKernelGGL((gemm_kernel<T, 256, 128, 8, 4, EpiNone>), g, dim3(512), 0, s, A, Bt, M, N,
+                         K, p.ks, w.ws, EpiNone{});
+      break;
+    }
+    case T128x128w8: {
+      dim3 g(N / 128, (M + 127) / 128, p.ks);
+      hipLaunchKernelGGL((gemm_kernel<T, 128, 128, 8, 4, EpiNone>), g, dim3(512), 0, s, A, Bt, M, N,
+                         K, p.ks, w.ws, EpiNone{});
+      break;
+    }
+    case T64x128w4: {
+      dim3 g(N / 128, (M + 63) / 64, p.ks);
+      hipLaunchKernelGGL((gemm_kernel<T, 64, 128, 4, 2, EpiNone>), g, dim3(256), 0, s, A, Bt, M, N,
+                         K, p.ks, w.ws, EpiNone{});
+      break;
+    }
+    default: {
+      dim3 g(N / 128, (M + 31) / 32, p.ks);
+      hipLaunchKernelGGL((gemm_kernel<T, 32, 128, 2, 1, EpiNone>), g, dim3(128), 0, s, A, Bt, M, N,
+                         K, p.ks, w.ws, EpiNone{});
+    }
+  }
+  return p.ks;
+}
+
+template <typename T>
+void gemm_bias_silu(const T* A, const T* Bt, const float* bias, T* out, int M, int N, int K,
+                    const GemmWork& w, hipStream_t s) {
+  run_gemm(A, Bt, M, N, K, w, EpiBiasSilu<T>{out, bias, N}, s);
+}
+template <typename T>
+void gemm_bias_f32(const T* A, const T* Bt, const float* bias, float* out, int M, int N, int K,
+                   const GemmWork& w, hipStream_t s) {
+  run_gemm(A, Bt, M, N, K, w, EpiBiasF32{out, bias, N}, s);
+}
+template <typename T>
+void gemm_qkv(const T* A, const T* Bt, const QkvArgs<T>& qa, int M, int N, int K,
+              const GemmWork& w, hipStream_t s) {
+  run_gemm(A, Bt, M, N, K, w, EpiQkv<T>{qa}, s);
+}
+template <typename T>
+void gemm_gated_resid(const T* A, const T* Bt, float* h, const float* mod, int mod_ld,
+                      int gate_off, int chunk_len, int M, int N, int K, const GemmWork& w,
+                      hipStream_t s) {
+  run_gemm(A, Bt, M, N, K, w, EpiGatedResid{h, mod, mod_ld, gate_off, chunk_len, N}, s);
+}
+template <typename T>
+void gemm_geglu(const T* A, const T* Bt, T* out, int M, int N, int K, const GemmWork& w,
+                hipStream_t s) {
+  run_gemm(A, Bt, M, N, K, w, EpiGeglu<T>{out, N / 2}, s);
+}
+template <typename T>
+void gemm_gelu(const T* A, const T* Bt, T* out, int M, int N, int K, const GemmWork& w,
+               hipStream_t s) {
+  run_gemm(A, Bt, M, N, K, w, EpiGelu<T>{out, N}, s);
+}
+
+#define FV_INSTANTIATE(T)                                                                        \
+  template void gemm_bias_silu<T>(const T*, const T*, const float*, T*, int, int, int,           \
+                                  const GemmWork&, hipStream_t);                                 \
+  template void gemm_bias_f32<T>(const T*, const T*, const float*, float*, int, int, int,        \
+                                 const GemmWork&, hipStream_t);                                  \
+  template void gemm_qkv<T>(const T*, const T*, const QkvArgs<T>&, int, int, int,                \
+                            const GemmWork&, hipStream_t);                                       \
+  template void gemm_gated_resid<T>(const T*, const T*, float*, const float*, int, int, int,     \
+                                    int, int, int, const GemmWork&, hipStream_t);                \
+  template void gemm_geglu<T>(const T*, const T*, T*, int, int, int, const GemmWork&,            \
+                              hipStream_t);                                                      \
+  template void gemm_gelu<T>(const T*, const T*, T*, int, int, int, const GemmWork&, hipStream_t); \
+  template int gemm_partials<T>(const T*, const T*, int, int, int, const GemmWork&, hipStream_t);
+FV_INSTANTIATE(bf16_t)
+FV_INSTANTIATE(float)
+#undef FV_INSTANTIATE
+
+}  // namespace fv

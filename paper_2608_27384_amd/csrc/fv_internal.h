@@ -1,0 +1,233 @@
+// Internal declarations of the gfx950 streaming action-decode library.
+//
+// Element types: "bf16" tensors hold raw bf16 bit patterns (uint16_t); every
+// kernel is written once as a template over the storage type T (bf16_t or
+// float) and uses the matching MFMA instruction (16x16x32 bf16 or 16x16x4
+// fp32), so both precisions share one code path.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "../../include/flashvla.h"
+
+namespace fv {
+
+typedef uint16_t bf16_t;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // 16-byte moves (native vector)
+
+// ---------------------------------------------------------------- conversions
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16_t x) { return __uint_as_float((uint32_t)x << 16); }
+
+// Round to nearest even (the gfx950 conversion instruction); NaN stays NaN.
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  return __builtin_bit_cast(bf16_t, static_cast<__bf16>(f));
+}
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) { return f32_to_bf16(x); }
+
+// ------------------------------------------------------------ MFMA operands
+// One 16x16 output tile: lane l holds rows 4*(l/16)+r (r = 0..3) of column
+// l%16.  An A-operand (B-operand) fragment holds KG consecutive k of row
+// (column) l%16 starting at k = KG*(l/16); one instruction covers KM = 4*KG k.
+template <typename T> struct Mfma;
+template <> struct Mfma<bf16_t> {
+  static constexpr int KG = 8, KM = 32;
+  typedef bf16x8 frag;
+  __device__ static __forceinline__ frag load(const bf16_t* p) {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(p));
+  }
+  __device__ static __forceinline__ f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct Mfma<float> {
+  static constexpr int KG = 1, KM = 4;
+  typedef float frag;
+  __device__ static __forceinline__ frag load(const float* p) { return *p; }
+  __device__ static __forceinline__ f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+};
+
+__device__ __forceinline__ float silu_f(float x) { return x / (1.0f + __expf(-x)); }
+__device__ __forceinline__ float gelu_tanh_f(float x) {
+  const float c = 0.7978845608028654f;  // sqrt(2/pi)
+  return 0.5f * x * (1.0f + tanhf(c * (x + 0.044715f * x * x * x)));
+}
+
+// ------------------------------------------------------------ GEMM launches
+// C[M][N] = A[M][K] * Bt[N][K]^T with fp32 accumulation, followed by a fused
+// epilogue.  A is row-major with leading dimension K; Bt is the weight stored
+// output-major ([out][in]).  Requirements: N % 128 == 0, K % 64 == 0 (bf16) or
+// K % 32 == 0 (fp32), 16-byte aligned base pointers.
+struct GemmPlan {
+  int tile = -1, ks = 1, tiles = 0;  // tile shape id, split-K factor, output tiles
+  size_t ws_floats = 0;              // split-K workspace this GEMM needs
+};
+GemmPlan plan_gemm(int M, int N, int K, bool bf16);
+
+// Split-K scratch shared by every GEMM of a handle (launches are stream
+// ordered): fp32 partial tiles.
+struct GemmWork {
+  float* ws = nullptr;
+};
+
+template <typename T>
+struct QkvArgs {
+  T* q;                 // [rows][Hq*dh] rotated queries
+  T* karena;            // this layer's keys   [Bmax][Hkv][S][dh]
+  T* vtarena;           // this layer's values [Bmax][Hkv][dh][S] (transposed)
+  const float* rcos;    // [S][dh/2]
+  const float* rsin;
+  const int2* row_pos;  // [rows] (stream b, arena row len[b] + token)
+  int tokens, n_q_heads, n_kv_heads, head_dim, S;
+};
+
+template <typename T>
+void gemm_bias_silu(const T* A, const T* Bt, const float* bias, T* out, int M, int N, int K,
+                    const GemmWork& w, hipStream_t s);
+template <typename T>
+void gemm_bias_f32(const T* A, const T* Bt, const float* bias, float* out, int M, int N, int K,
+                   const GemmWork& w, hipStream_t s);
+template <typename T>
+void gemm_qkv(const T* A, const T* Bt, const QkvArgs<T>& qa, int M, int N, int K,
+              const GemmWork& w, hipStream_t s);
+// h[row][col] += mod[row / chunk_len][gate_off + col] * acc
+template <typename T>
+void gemm_gated_resid(const T* A, const T* Bt, float* h, const float* mod, int mod_ld,
+                      int gate_off, int chunk_len, int M, int N, int K, const GemmWork& w,
+                      hipStream_t s);
+// out[row][n] = gelu(acc_gate) * acc_up   (packed columns, N = 2F)
+template <typename T>
+void gemm_geglu(const T* A, const T* Bt, T* out, int M, int N, int K, const GemmWork& w,
+                hipStream_t s);
+template <typename T>
+void gemm_gelu(const T* A, const T* Bt, T* out, int M, int N, int K, const GemmWork& w,
+               hipStream_t s);
+// Split-K GEMM that only writes its fp32 partials [KS][M][N] to w.ws; returns
+// KS, or 1 (nothing launched) when the plan does not split k.
+template <typename T>
+int gemm_partials(const T* A, const T* Bt, int M, int N, int K, const GemmWork& w,
+                  hipStream_t s);
+
+// ------------------------------------------------------------ other kernels
+template <typename T>
+void launch_time_embed(const float* t, T* e, int rows, int width, hipStream_t s);
+template <typename T>
+void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, float* h,
+                         const float* mod, int mod_ld, int chunk_len, float eps, T* u, int rows,
+                         int A, int W, hipStream_t s);
+// h += gate * sum_z part[z] (split order); then, if norm_off >= 0,
+// u = rmsnorm(h) (1 + scale) + shift with the modulation at norm_off.
+template <typename T>
+void launch_resid_norm(const float* part, int ks, float* h, const float* mod, int mod_ld,
+                       int gate_off, int norm_off, int chunk_len, float eps, T* u, int rows,
+                       int W, hipStream_t s);
+void launch_row_pos(const int* len, int2* row_pos, int rows, int tokens, hipStream_t s);
+template <typename T>
+void launch_adarms(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
+                   float eps, T* u, int rows, int W, hipStream_t s);
+void launch_final(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
+                  float eps, const float* w_out, const float* b_out, float* v, int rows, int W,
+                  int A, hipStream_t s);
+void launch_euler_shift(float* buffer, const float* t, const float* v, float* out,
+                        const uint64_t* noise_state, uint32_t* ticket, int B, int K, int CA,
+                        hipStream_t s);
+void launch_seq_euler(float* x, const float* v, const float* tsched, int j, int n, hipStream_t s);
+void launch_copy_f32(float* dst, const float* src, size_t n, hipStream_t s);
+void launch_fill_t(float* t, const float* tsched, int j, int B, hipStream_t s);
+template <typename T>
+void launch_prefix_copy(const T* k, const T* v, int L, int B, int ld, int Hkv, int dh,
+                        T* karena, T* vtarena, int Bmax, int S, const int* len, hipStream_t s);
+
+struct AttnArgs {
+  const void* q;        // [B*tokens][Hq][dh]
+  const void* karena;   // layer base [Bmax][Hkv][S][dh]
+  const void* vtarena;  // layer base [Bmax][Hkv][dh][S]
+  const int* len;
+  void* o;              // [B*tokens][Hq*dh]
+  float* part_o;        // [n_split][B*tokens*Hq][dh]
+  float* part_ml;       // [n_split][B*tokens*Hq][2]
+  int B, tokens, chunk_len, n_q_heads, n_kv_heads, head_dim, S, n_split;
+};
+template <typename T>
+void launch_attention(const AttnArgs& a, hipStream_t s);
+template <typename T>
+int attention_row_tiles(int tokens, int n_q_heads, int n_kv_heads);
+
+// ------------------------------------------------------------------- handle
+struct GraphEntry {
+  int kind = 0, batch = 0, n = 0;
+  const void* p[4] = {nullptr, nullptr, nullptr, nullptr};
+  hipGraphExec_t exec = nullptr;
+  uint64_t last_use = 0;
+};
+
+struct Handle {
+  fv_cfg cfg{};
+  int device = 0;
+  bool bf16 = true;
+  int L = 0, W = 0, Hq = 0, Hkv = 0, dh = 0, F = 0, A = 0, C = 0, K = 0, T = 0;
+  int Pmax = 0, Bmax = 0, S = 0;   // S: arena rows per (layer, stream, kv head)
+  int Nqkv = 0, Nmod = 0, Ngu = 0;
+  size_t esz = 2;                  // element size of T
+
+  // packed weights (device)
+  float* w_in = nullptr;  float* b_in = nullptr;   // fp32 [A][W], [W]
+  void* w_t1 = nullptr;   float* b_t1 = nullptr;   // T [W][W] (out-major)
+  void* w_t2 = nullptr;   float* b_t2 = nullptr;
+  void* w_mod = nullptr;  float* b_mod = nullptr;  // T [Nmod][W], fp32 [Nmod]
+  std::vector<void*> wqkv, wo, wgu, wd;            // T, out-major
+  float* w_out = nullptr; float* b_out = nullptr;  // fp32 [W][A], [A]
+
+  // prefix arena and lengths
+  void* karena = nullptr;   // [L][Bmax][Hkv][S][dh]
+  void* vtarena = nullptr;  // [L][Bmax][Hkv][dh][S]
+  int* d_len = nullptr;
+  std::vector<int32_t> len_host;
+  int batch = 0;
+  bool prefix_set = false;
+
+  // rotary tables [S][dh/2]
+  float* rcos = nullptr; float* rsin = nullptr;
+
+  // scratch
+  void* e = nullptr; void* hid = nullptr; void* cond = nullptr;  // T [Bmax*K][W]
+  float* mod = nullptr;                                           // [Bmax*K][Nmod]
+  float* hres = nullptr;                                          // [Bmax*T][W]
+  void* u = nullptr;                                              // T [Bmax*T][W]
+  void* q = nullptr; void* o = nullptr;                           // T [Bmax*T][Hq*dh]
+  void* m = nullptr;                                              // T [Bmax*T][F]
+  float* v = nullptr;                                             // [Bmax][K][C][A]
+  int2* row_pos = nullptr;                                        // [Bmax*T]
+  float* part_o = nullptr; float* part_ml = nullptr; int max_split = 1;
+  float* seq_x = nullptr; float* seq_t = nullptr;
+  std::vector<std::pair<int, float*>> tscheds;  // sequential-decode t_j tables by step count
+
+  GemmWork gw;                    // split-K workspace and counters
+  uint64_t* d_noise = nullptr;   // {seed, step}
+  uint32_t* d_ticket = nullptr;
+
+  // graphs
+  bool use_graphs = true;
+  hipStream_t cap_stream = nullptr;
+  std::vector<GraphEntry> graphs;
+  uint64_t use_clock = 0;
+
+  std::string last_error;
+  std::vector<void*> allocations;
+};
+
+}  // namespace fv

@@ -1,0 +1,528 @@
+// Element-wise and row-wise kernels of the decode step.
+#include "fv_internal.h"
+
+namespace fv {
+
+namespace {
+
+constexpr double kTwoPi = 6.283185307179586476925286766559;
+
+// ------------------------------------------------------------------ helpers
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+// -------------------------------------------------------- time embedding
+// e[row] = [sin(2 pi t / p_i) | cos(2 pi t / p_i)], p_i = 4e-3 * (4/4e-3)^(i/(W/2-1)),
+// evaluated in fp64 (the timestep embedding that drives FiLM, Appendix
+// "Model architecture").
+template <typename T>
+__global__ void time_embed_kernel(const float* __restrict__ t, T* __restrict__ e, int rows,
+                                  int width) {
+  const int half = width / 2;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= rows * half) return;
+  const int row = idx / half, i = idx - row * half;
+  const double period = 4e-3 * pow(4.0 / 4e-3, (double)i / (double)(half - 1));
+  const double ang = kTwoPi * (double)t[row] / period;
+  double sv, cv;
+  sincos(ang, &sv, &cv);
+  e[(size_t)row * width + i] = from_f32<T>((float)sv);
+  e[(size_t)row * width + half + i] = from_f32<T>((float)cv);
+}
+
+// ---------------------------------- action embedding + first FiLM RMSNorm
+// h[row] = x[row] w_in + b_in (fp32), then u[row] = rmsnorm(h) (1 + scale) +
+// shift with norm 0's modulation of the row's chunk.  A block takes
+// kEmbRows rows; thread t owns 4 consecutive columns (per 1024-column chunk)
+// of every row, reads w_in once for all rows and keeps the x rows in LDS.
+constexpr int kEmbRows = 8;
+
+__device__ __forceinline__ float block_sum_256(float v, float* red) {
+  v = wave_sum(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return red[0] + red[1] + red[2] + red[3];
+}
+
+template <typename T>
+__device__ __forceinline__ void store4(T* p, float a, float b, float c, float d);
+template <>
+__device__ __forceinline__ void store4<float>(float* p, float a, float b, float c, float d) {
+  *reinterpret_cast<f32x4*>(p) = f32x4{a, b, c, d};
+}
+template <>
+__device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float a, float b, float c, float d) {
+  *reinterpret_cast<u16x4*>(p) = u16x4{f32_to_bf16(a), f32_to_bf16(b), f32_to_bf16(c), f32_to_bf16(d)};
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void embed_adarms_kernel(
+    const float* __restrict__ x, const float* __restrict__ w_in, const float* __restrict__ b_in,
+    float* __restrict__ h, const float* __restrict__ mod, int mod_ld, int chunk_len, float eps,
+    T* __restrict__ u, int rows, int A, int W) {
+  __shared__ float sx[kEmbRows][64];
+  __shared__ float sred[kEmbRows][4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row0 = blockIdx.x * kEmbRows;
+  for (int idx = tid; idx < kEmbRows * A; idx += 256) {
+    const int r = idx / A, a = idx - r * A;
+    sx[r][a] = row0 + r < rows ? x[(size_t)(row0 + r) * A + a] : 0.f;
+  }
+  __syncthreads();
+  float ss[kEmbRows];
+#pragma unroll
+  for (int r = 0; r < kEmbRows; ++r) ss[r] = 0.f;
+  for (int c = 4 * tid; c < W; c += 1024) {
+    f32x4 acc[kEmbRows];
+    const f32x4 bias = *reinterpret_cast<const f32x4*>(b_in + c);
+#pragma unroll
+    for (int r = 0; r < kEmbRows; ++r) acc[r] = bias;
+    for (int a = 0; a < A; ++a) {
+      const f32x4 wv = *reinterpret_cast<const f32x4*>(w_in + (size_t)a * W + c);
+#pragma unroll
+      for (int r = 0; r < kEmbRows; ++r) {
+        const float xv = sx[r][a];
+        acc[r] += xv * wv;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kEmbRows; ++r) {
+      if (row0 + r < rows) *reinterpret_cast<f32x4*>(h + (size_t)(row0 + r) * W + c) = acc[r];
+      ss[r] += acc[r][0] * acc[r][0] + acc[r][1] * acc[r][1] + acc[r][2] * acc[r][2] +
+               acc[r][3] * acc[r][3];
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kEmbRows; ++r) {
+    const float v = wave_sum(ss[r]);
+    if (lane == 0) sred[r][wave] = v;
+  }
+  __syncthreads();
+  for (int c = 4 * tid; c < W; c += 1024) {
+#pragma unroll
+    for (int r = 0; r < kEmbRows; ++r) {
+      const int row = row0 + r;
+      if (row >= rows) break;
+      const float tot = sred[r][0] + sred[r][1] + sred[r][2] + sred[r][3];
+      const float rinv = 1.0f / sqrtf(tot / (float)W + eps);
+      const f32x4 hv = *reinterpret_cast<const f32x4*>(h + (size_t)row * W + c);
+      const float* sc = mod + (size_t)(row / chunk_len) * mod_ld;
+      const f32x4 sv = *reinterpret_cast<const f32x4*>(sc + c);
+      const f32x4 bv = *reinterpret_cast<const f32x4*>(sc + W + c);
+      store4<T>(u + (size_t)row * W + c, hv[0] * rinv * (1.0f + sv[0]) + bv[0],
+                hv[1] * rinv * (1.0f + sv[1]) + bv[1], hv[2] * rinv * (1.0f + sv[2]) + bv[2],
+                hv[3] * rinv * (1.0f + sv[3]) + bv[3]);
+    }
+  }
+}
+
+// --------------------------------------- gated residual + next FiLM RMSNorm
+// One block per row: h[row] += gate[chunk] * sum_z part[z][row] (split order),
+// then (norm_off >= 0) u[row] = rmsnorm(h) (1 + scale) + shift.
+template <typename T>
+__global__ __launch_bounds__(256) void resid_norm_kernel(const float* __restrict__ part, int ks,
+                                                         float* __restrict__ h,
+                                                         const float* __restrict__ mod,
+                                                         int mod_ld, int gate_off, int norm_off,
+                                                         int chunk_len, float eps,
+                                                         T* __restrict__ u, int rows, int W) {
+  __shared__ float red[4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const float* mrow = mod + (size_t)(row / chunk_len) * mod_ld;
+  f32x4 hq[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  float ss = 0.f;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int c = 4 * tid + 1024 * q;
+    if (c < W) {
+      f32x4 acc = *reinterpret_cast<const f32x4*>(part + (size_t)row * W + c);
+      for (int z = 1; z < ks; ++z)
+        acc += *reinterpret_cast<const f32x4*>(part + ((size_t)z * rows + row) * W + c);
+      const f32x4 g = *reinterpret_cast<const f32x4*>(mrow + gate_off + c);
+      f32x4 hv = *reinterpret_cast<const f32x4*>(h + (size_t)row * W + c);
+      hv += g * acc;
+      *reinterpret_cast<f32x4*>(h + (size_t)row * W + c) = hv;
+      hq[q] = hv;
+      ss += hv[0] * hv[0] + hv[1] * hv[1] + hv[2] * hv[2] + hv[3] * hv[3];
+    }
+  }
+  if (norm_off < 0) return;
+  const float rinv = 1.0f / sqrtf(block_sum_256(ss, red) / (float)W + eps);
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int c = 4 * tid + 1024 * q;
+    if (c < W) {
+      const f32x4 sv = *reinterpret_cast<const f32x4*>(mrow + norm_off + c);
+      const f32x4 bv = *reinterpret_cast<const f32x4*>(mrow + norm_off + W + c);
+      const f32x4 hv = hq[q];
+      store4<T>(u + (size_t)row * W + c, hv[0] * rinv * (1.0f + sv[0]) + bv[0],
+                hv[1] * rinv * (1.0f + sv[1]) + bv[1], hv[2] * rinv * (1.0f + sv[2]) + bv[2],
+                hv[3] * rinv * (1.0f + sv[3]) + bv[3]);
+    }
+  }
+}
+
+// (stream, arena row) of every token row: b = row / tokens, len[b] + token.
+__global__ void row_pos_kernel(const int* __restrict__ len, int2* __restrict__ row_pos, int rows,
+                               int tokens) {
+  const int row = blockIdx.x * blockDim.x + threadIdx.x;
+  if (row >= rows) return;
+  const int b = row / tokens;
+  row_pos[row] = make_int2(b, len[b] + (row - b * tokens));
+}
+
+// -------------------------------------------------- FiLM-conditioned RMSNorm
+// u = h / sqrt(mean(h^2) + eps) * (1 + scale[chunk]) + shift[chunk]; one wave per row.
+template <typename T>
+__global__ __launch_bounds__(256) void adarms_kernel(const float* __restrict__ h,
+                                                     const float* __restrict__ mod, int mod_ld,
+                                                     int scale_off, int chunk_len, float eps,
+                                                     T* __restrict__ u, int rows, int W) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const float* hr = h + (size_t)row * W;
+  float ss = 0.f;
+  for (int c = lane * 4; c < W; c += 256) {
+    const float4 x = *reinterpret_cast<const float4*>(hr + c);
+    ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+  }
+  ss = wave_sum(ss);
+  const float rinv = 1.0f / sqrtf(ss / (float)W + eps);
+  const float* sc = mod + (size_t)(row / chunk_len) * mod_ld + scale_off;
+  const float* sh = sc + W;
+  T* ur = u + (size_t)row * W;
+  for (int c = lane * 4; c < W; c += 256) {
+    const float4 x = *reinterpret_cast<const float4*>(hr + c);
+    const float4 s = *reinterpret_cast<const float4*>(sc + c);
+    const float4 b = *reinterpret_cast<const float4*>(sh + c);
+    ur[c + 0] = from_f32<T>(x.x * rinv * (1.0f + s.x) + b.x);
+    ur[c + 1] = from_f32<T>(x.y * rinv * (1.0f + s.y) + b.y);
+    ur[c + 2] = from_f32<T>(x.z * rinv * (1.0f + s.z) + b.z);
+    ur[c + 3] = from_f32<T>(x.w * rinv * (1.0f + s.w) + b.w);
+  }
+}
+
+// ------------------------------------- final FiLM RMSNorm + velocity head
+// v[row] = (rmsnorm(h) (1 + scale) + shift) w_out + b_out, fp32.  A block
+// handles kFinalRows rows: each wave normalises one row into LDS.  w_out is
+// then staged through LDS 128 rows at a time; each output (row, a) is summed
+// by `parts` threads over interleaved slices of every chunk, and the slices
+// are added in a fixed order.
+constexpr int kFinalRows = 4;
+constexpr int kFinalChunk = 128;
+__global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ h,
+                                                    const float* __restrict__ mod, int mod_ld,
+                                                    int scale_off, int chunk_len, float eps,
+                                                    const float* __restrict__ w_out,
+                                                    const float* __restrict__ b_out,
+                                                    float* __restrict__ v, int rows, int W,
+                                                    int A) {
+  extern __shared__ float smem[];  // su [kFinalRows][W], sw [kFinalChunk][A], sp [256]
+  float* su = smem;
+  float* sw = su + kFinalRows * W;
+  float* sp = sw + kFinalChunk * A;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, tid = threadIdx.x;
+  const int row0 = blockIdx.x * kFinalRows;
+  {
+    const int row = row0 + wave;
+    if (row < rows) {
+      const float* hr = h + (size_t)row * W;
+      float ss = 0.f;
+      for (int c = lane; c < W; c += 64) ss += hr[c] * hr[c];
+      ss = wave_sum(ss);
+      const float rinv = 1.0f / sqrtf(ss / (float)W + eps);
+      const float* sc = mod + (size_t)(row / chunk_len) * mod_ld + scale_off;
+      for (int c = lane; c < W; c += 64)
+        su[wave * W + c] = hr[c] * rinv * (1.0f + sc[c]) + sc[W + c];
+    } else {
+      for (int c = lane; c < W; c += 64) su[wave * W + c] = 0.f;
+    }
+  }
+  const int nout = kFinalRows * A;  // <= 256
+  const int parts = 256 / nout;
+  const int o = tid % nout, part = tid / nout;
+  const int r = o / A, a = o - r * A;
+  float acc4[4] = {0.f, 0.f, 0.f, 0.f};  // independent chains keep LDS loads in flight
+  for (int n0 = 0; n0 < W; n0 += kFinalChunk) {
+    __syncthreads();
+    for (int i = tid; i < kFinalChunk * A; i += 256) sw[i] = w_out[(size_t)n0 * A + i];
+    __syncthreads();
+    if (part < parts) {
+      const float* ur = su + r * W + n0;
+#pragma unroll 8
+      for (int nn = part; nn < kFinalChunk; nn += parts)
+        acc4[nn & 3] = fmaf(ur[nn], sw[nn * A + a], acc4[nn & 3]);
+    }
+  }
+  sp[tid] = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
+  __syncthreads();
+  if (tid < nout) {
+    float tot = b_out[a];
+    for (int p = 0; p < parts; ++p) tot += sp[p * nout + tid];
+    if (row0 + r < rows) v[(size_t)(row0 + r) * A + a] = tot;
+  }
+}
+
+// ------------------------------------------------------------ Philox4x32-10
+__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+  const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+  const uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += W0;
+      k1 += W1;
+    }
+    const uint32_t hi0 = __umulhi(M0, c[0]), lo0 = M0 * c[0];
+    const uint32_t hi1 = __umulhi(M1, c[2]), lo1 = M1 * c[2];
+    const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = lo1;
+    c[2] = n2;
+    c[3] = lo0;
+  }
+}
+
+__device__ __forceinline__ void box_muller(uint32_t r0, uint32_t r1, float* z0, float* z1) {
+  const double u0 = ((double)r0 + 0.5) * 2.3283064365386962890625e-10;  // 2^-32
+  const double u1 = ((double)r1 + 0.5) * 2.3283064365386962890625e-10;
+  const double rad = sqrt(-2.0 * log(u0));
+  double s, c;
+  sincos(kTwoPi * u1, &s, &c);
+  *z0 = (float)(rad * c);
+  *z1 = (float)(rad * s);
+}
+
+// ------------------------------------------- Euler + emit + shift + refill
+// Thread (j, k) owns group j of 4 consecutive elements of the [C][A] chunk in
+// slot k of stream b; all K slots of a group live in one block.  Every thread
+// loads its slot and applies x'_k = x_k - dt_k v_k (rounded product, rounded
+// difference); after a barrier slot 0 writes the emitted chunk, slot k >= 1
+// writes buffer[k-1], and slot K-1 also writes fresh noise into buffer[K-1].
+// All loads precede the barrier and all stores follow it, so the in-place
+// shift has no race.  The last block to finish advances the step counter.
+__global__ __launch_bounds__(256) void euler_shift_kernel(float* __restrict__ buf,
+                                                          const float* __restrict__ t,
+                                                          const float* __restrict__ v,
+                                                          float* __restrict__ out,
+                                                          uint64_t* __restrict__ noise_state,
+                                                          uint32_t* __restrict__ ticket, int B,
+                                                          int K, int CA) {
+  // The update must round the product and the difference separately.
+#pragma clang fp contract(off)
+  const int groups = (CA + 3) >> 2;
+  const int gpb = 256 / K;                      // element groups per block
+  const int k = threadIdx.x % K, jl = threadIdx.x / K;
+  const int gid = blockIdx.x * gpb + jl;        // global group index over (b, j)
+  const uint64_t seed = noise_state[0], step = noise_state[1];
+  const bool active = jl < gpb && gid < B * groups;
+  float xn[4] = {0.f, 0.f, 0.f, 0.f};
+  int b = 0, j = 0, e0 = 0, ne = 0;
+  if (active) {
+    b = gid / groups;
+    j = gid - b * groups;
+    e0 = 4 * j;
+    ne = min(4, CA - e0);
+    const float tk = t[(size_t)b * K + k];
+    const float tp = k > 0 ? t[(size_t)b * K + k - 1] : 0.f;
+    const float dt = tk - tp;
+    const size_t base = ((size_t)b * K + k) * CA + e0;
+    for (int i = 0; i < ne; ++i) {
+      const float p = dt * v[base + i];
+      xn[i] = buf[base + i] - p;
+    }
+  }
+  __syncthreads();
+  if (active) {
+    const size_t base = ((size_t)b * K + k) * CA + e0;
+    if (k == 0) {
+      for (int i = 0; i < ne; ++i) out[(size_t)b * CA + e0 + i] = xn[i];
+    } else {
+      for (int i = 0; i < ne; ++i) buf[base - CA + i] = xn[i];
+    }
+    if (k == K - 1) {
+      uint32_t c[4] = {(uint32_t)j, (uint32_t)step, (uint32_t)(step >> 32), 0u};
+      const uint64_t sb = seed + (uint64_t)b;
+      philox4x32_10(c, (uint32_t)sb, (uint32_t)(sb >> 32));
+      float z[4];
+      box_muller(c[0], c[1], &z[0], &z[1]);
+      box_muller(c[2], c[3], &z[2], &z[3]);
+      for (int i = 0; i < ne; ++i) buf[base + i] = z[i];
+    }
+  }
+  // step counter: advanced once every block has read it
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t done =
+        __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    if (done == gridDim.x - 1) {
+      noise_state[1] = step + 1;
+      __hip_atomic_store(ticket, 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+// x <- x - (t_j - t_{j+1}) v   (sequential decode; product then difference rounded)
+__global__ void seq_euler_kernel(float* __restrict__ x, const float* __restrict__ v,
+                                 const float* __restrict__ tsched, int j, int n) {
+#pragma clang fp contract(off)
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n) return;
+  const float dt = tsched[j] - tsched[j + 1];
+  const float p = dt * v[idx];
+  x[idx] = x[idx] - p;
+}
+
+__global__ void copy_f32_kernel(float* __restrict__ d, const float* __restrict__ s, size_t n) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) d[i] = s[i];
+}
+
+__global__ void fill_t_kernel(float* __restrict__ t, const float* __restrict__ tsched, int j,
+                              int B) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < B) t[i] = tsched[j];
+}
+
+// ---------------------------------------------------------- prefix install
+// k: [L][B][ld][Hkv][dh] -> karena [L][Bmax][Hkv][S][dh], rows p < len[b];
+// v: same source layout -> vtarena [L][Bmax][Hkv][dh][S] through a 64x64 LDS
+// transpose (p-major reads and d-major writes are both coalesced).
+template <typename T>
+__global__ __launch_bounds__(256) void prefix_copy_kernel(const T* __restrict__ k,
+                                                          const T* __restrict__ v, int B,
+                                                          int ld, int Hkv, int dh,
+                                                          T* __restrict__ karena,
+                                                          T* __restrict__ vtarena, int Bmax,
+                                                          int S, const int* __restrict__ len) {
+  __shared__ T tile[64][65];
+  const int pt = blockIdx.x, dt = blockIdx.y;
+  const int lbg = blockIdx.z;  // (l, b, g)
+  const int g = lbg % Hkv, lb = lbg / Hkv, b = lb % B, l = lb / B;
+  const int n = len[b];
+  const int p0 = pt * 64, d0 = dt * 64;
+  if (p0 >= n) return;
+  const size_t src_base = (((size_t)l * B + b) * ld) * Hkv * dh;
+  const size_t kdst = (((size_t)l * Bmax + b) * Hkv + g) * (size_t)S * dh;
+  const size_t vdst = (((size_t)l * Bmax + b) * Hkv + g) * (size_t)dh * S;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int pp = ty; pp < 64; pp += 4) {
+    const int p = p0 + pp, d = d0 + tx;
+    if (p < n && d < dh) {
+      const size_t si = src_base + ((size_t)p * Hkv + g) * dh + d;
+      karena[kdst + (size_t)p * dh + d] = k[si];
+      tile[pp][tx] = v[si];
+    }
+  }
+  __syncthreads();
+  for (int dd = ty; dd < 64; dd += 4) {
+    const int d = d0 + dd, p = p0 + tx;
+    if (p < n && d < dh) vtarena[vdst + (size_t)d * S + p] = tile[tx][dd];
+  }
+}
+
+}  // namespace
+
+template <typename T>
+void launch_time_embed(const float* t, T* e, int rows, int width, hipStream_t s) {
+  const int n = rows * (width / 2);
+  hipLaunchKernelGGL((time_embed_kernel<T>), dim3((n + 255) / 256), dim3(256), 0, s, t, e, rows,
+                     width);
+}
+
+template <typename T>
+void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, float* h,
+                         const float* mod, int mod_ld, int chunk_len, float eps, T* u, int rows,
+                         int A, int W, hipStream_t s) {
+  hipLaunchKernelGGL((embed_adarms_kernel<T>), dim3((rows + kEmbRows - 1) / kEmbRows), dim3(256),
+                     0, s, x, w_in, b_in, h, mod, mod_ld, chunk_len, eps, u, rows, A, W);
+}
+
+template <typename T>
+void launch_resid_norm(const float* part, int ks, float* h, const float* mod, int mod_ld,
+                       int gate_off, int norm_off, int chunk_len, float eps, T* u, int rows,
+                       int W, hipStream_t s) {
+  hipLaunchKernelGGL((resid_norm_kernel<T>), dim3(rows), dim3(256), 0, s, part, ks, h, mod,
+                     mod_ld, gate_off, norm_off, chunk_len, eps, u, rows, W);
+}
+
+void launch_row_pos(const int* len, int2* row_pos, int rows, int tokens, hipStream_t s) {
+  hipLaunchKernelGGL(row_pos_kernel, dim3((rows + 255) / 256), dim3(256), 0, s, len, row_pos,
+                     rows, tokens);
+}
+
+template <typename T>
+void launch_adarms(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
+                   float eps, T* u, int rows, int W, hipStream_t s) {
+  hipLaunchKernelGGL((adarms_kernel<T>), dim3((rows + 3) / 4), dim3(256), 0, s, h, mod, mod_ld,
+                     scale_off, chunk_len, eps, u, rows, W);
+}
+
+void launch_final(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
+                  float eps, const float* w_out, const float* b_out, float* v, int rows, int W,
+                  int A, hipStream_t s) {
+  const size_t lds = (size_t)(kFinalRows * W + kFinalChunk * A + 256) * sizeof(float);
+  hipLaunchKernelGGL(final_kernel, dim3((rows + kFinalRows - 1) / kFinalRows), dim3(256), lds, s, h, mod, mod_ld,
+                     scale_off, chunk_len, eps, w_out, b_out, v, rows, W, A);
+}
+
+void launch_euler_shift(float* buffer, const float* t, const float* v, float* out,
+                        const uint64_t* noise_state, uint32_t* ticket, int B, int K, int CA,
+                        hipStream_t s) {
+  const int groups = (CA + 3) / 4;
+  const int gpb = 256 / K;
+  const int n = B * groups;
+  hipLaunchKernelGGL(euler_shift_kernel, dim3((n + gpb - 1) / gpb), dim3(256), 0, s, buffer, t, v,
+                     out, const_cast<uint64_t*>(noise_state), ticket, B, K, CA);
+}
+
+void launch_seq_euler(float* x, const float* v, const float* tsched, int j, int n,
+                      hipStream_t s) {
+  hipLaunchKernelGGL(seq_euler_kernel, dim3((n + 255) / 256), dim3(256), 0, s, x, v, tsched, j,
+                     n);
+}
+
+void launch_copy_f32(float* dst, const float* src, size_t n, hipStream_t s) {
+  hipLaunchKernelGGL(copy_f32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, dst,
+                     src, n);
+}
+
+void launch_fill_t(float* t, const float* tsched, int j, int B, hipStream_t s) {
+  hipLaunchKernelGGL(fill_t_kernel, dim3((B + 255) / 256), dim3(256), 0, s, t, tsched, j, B);
+}
+
+template <typename T>
+void launch_prefix_copy(const T* k, const T* v, int L, int B, int ld, int Hkv, int dh,
+                        T* karena, T* vtarena, int Bmax, int S, const int* len, hipStream_t s) {
+  dim3 grid((ld + 63) / 64, (dh + 63) / 64, L * B * Hkv);
+  hipLaunchKernelGGL((prefix_copy_kernel<T>), grid, dim3(256), 0, s, k, v, B, ld, Hkv, dh,
+                     karena, vtarena, Bmax, S, len);
+}
+
+template void launch_time_embed<bf16_t>(const float*, bf16_t*, int, int, hipStream_t);
+template void launch_time_embed<float>(const float*, float*, int, int, hipStream_t);
+template void launch_embed_adarms<bf16_t>(const float*, const float*, const float*, float*,
+                                          const float*, int, int, float, bf16_t*, int, int, int,
+                                          hipStream_t);
+template void launch_embed_adarms<float>(const float*, const float*, const float*, float*,
+                                         const float*, int, int, float, float*, int, int, int,
+                                         hipStream_t);
+template void launch_resid_norm<bf16_t>(const float*, int, float*, const float*, int, int, int,
+                                        int, float, bf16_t*, int, int, hipStream_t);
+template void launch_resid_norm<float>(const float*, int, float*, const float*, int, int, int,
+                                       int, float, float*, int, int, hipStream_t);
+template void launch_adarms<bf16_t>(const float*, const float*, int, int, int, float, bf16_t*,
+                                    int, int, hipStream_t);
+template void launch_adarms<float>(const float*, const float*, int, int, int, float, float*, int,
+                                   int, hipStream_t);
+template void launch_prefix_copy<bf16_t>(const bf16_t*, const bf16_t*, int, int, int, int, int,
+                                         bf16_t*, bf16_t*, int, int, const int*, hipStream_t);
+template void launch_prefix_copy<float>(const float*, const float*, int, int, int, int, int,
+                                        float*, float*, int, int, const int*, hipStream_t);
+
+}  // namespace fv

@@ -97,7 +97,7 @@ WORKLOADS: Dict[str, Workload] = {
     "small_bf16": Workload("small_bf16", 2, 256, 4, 1, 64, 512, 32, 12, 4, 70, 1, BF16),
     "small_bf16_b3": Workload("small_bf16_b3", 2, 256, 4, 2, 128, 768, 32, 10, 3,
                               (0, 90), 3, BF16),
-    "small_fp32_b2": Workload("small_fp32_b2", 2, 128, 4, 2, 32, 256, 8, 6, 5,
+    "small_fp32_b2": Workload("small_fp32_b2", 2, 128, 4, 2, 64, 256, 8, 6, 5,
                               (3, 40), 2, FP32),
 }
 

@@ -1,0 +1,175 @@
+"""GPU parity: the HIP path against the CPU oracle on the same seeded inputs.
+
+Velocities and emitted chunks are compared per (stream, chunk) slice as
+max|gpu - oracle| / max|oracle|, within 1e-4 in fp32 mode and 1e-2 in bf16
+mode.  Buffer bookkeeping (slot shift, emission, noise refill) is compared
+bit for bit against the oracle's fp32 replica of the queue update applied to
+the GPU's own velocity.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_util import Case, dev, host, rel_err, tol
+
+pytestmark = pytest.mark.gpu
+
+SMALL = ["tiny_fp32", "small_fp32_b2", "small_bf16", "small_bf16_b3"]
+
+
+def _stage_report(case):
+    """Per-stage errors (FiLM params, embedding, each layer) for diagnosis."""
+    import torch
+    w = case.w
+    B, T, W, L = w.batch, w.tokens, w.width, w.n_layers
+    lines = []
+    hd = torch.empty((B, T, W), dtype=torch.float32, device="cuda")
+    md = torch.empty((B, w.n_chunks, (6 * L + 2) * W), dtype=torch.float32, device="cuda")
+    for b in range(B):
+        tr = {}
+        oracle.velocity(case.x[b], case.t[b], case.k[:, b], case.v[:, b], int(case.lens[b]),
+                        case.W, w, trace=tr)
+        case.ex.debug_forward(case.xd, case.td, 0, hd, md)
+        mod = host(md)[b]
+        for n in range(2 * L + 1):
+            for j in range(3 if n < 2 * L else 2):
+                got = mod[:, 3 * W * n + W * j: 3 * W * n + W * (j + 1)]
+                ref = tr["mods"][n][j][::w.chunk_len]
+                lines.append(f"b{b} mod n{n} j{j}: {rel_err(got, ref):.2e}")
+        h0 = case.x[b].reshape(T, -1).astype(np.float64) @ case.W["w_in"] + case.W["b_in"]
+        lines.append(f"b{b} embed: {rel_err(host(hd)[b], h0):.2e}")
+        for l in range(L):
+            case.ex.debug_forward(case.xd, case.td, l + 1, hd)
+            lines.append(f"b{b} layer {l}: {rel_err(host(hd)[b], tr['h'][l]):.2e}")
+    return "\n".join(lines)
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_velocity_parity_small(name):
+    w = synth.workload(name)
+    case = Case(w)
+    try:
+        v = case.gpu_velocity()
+        errs = []
+        for b in range(w.batch):
+            ref = case.oracle_velocity(b)
+            errs += [rel_err(v[b, k], ref[k]) for k in range(w.n_chunks)]
+        if max(errs) > tol(w):
+            pytest.fail(f"max rel err {max(errs):.3e} > {tol(w)}\n" + _stage_report(case))
+        print(name, "max rel err", max(errs))
+    finally:
+        case.close()
+
+
+def test_decode_steps_lockstep_tiny():
+    """Eight decode steps of the tiny fp32 config; each step the oracle takes
+    the GPU's pre-step buffer, so errors do not compound."""
+    w = synth.workload("tiny_fp32")
+    case = Case(w, noise_seed=5)
+    try:
+        xd = case.xd
+        for s in range(8):
+            pre = host(xd).copy()
+            case.ex.decode_step(xd, case.td, case.out)
+            post, out = host(xd), host(case.out)
+            new, ref_out = oracle.decode_step(pre, case.t, case.k, case.v, case.lens, case.W, w,
+                                              noise_seed=5, step=s)
+            assert rel_err(out[0], ref_out[0]) < tol(w), s
+            for k in range(w.n_chunks - 1):
+                assert rel_err(post[0, k], new[0, k]) < tol(w), (s, k)
+            # fresh noise: same Philox draw as the oracle (fp64 Box-Muller on both sides)
+            z = oracle.gaussian_chunk(5, s, w.chunk_len, w.action_dim)
+            assert np.max(np.abs(post[0, -1] - z)) <= 1e-6, s
+        assert case.ex.noise_state == (5, 8)
+    finally:
+        case.close()
+
+
+@pytest.mark.parametrize("name", ["tiny_fp32", "small_bf16_b3"])
+def test_bookkeeping_bit_exact(name):
+    """After a step the buffer and emitted chunk equal, bit for bit, the fp32
+    queue update (rounded product, rounded difference, shift, refill) applied
+    to the GPU's own velocity; the refill equals the oracle's Philox draw."""
+    w = synth.workload(name)
+    case = Case(w, noise_seed=123)
+    try:
+        case.ex.set_noise_state(123, 2**32 + 7)
+        v = case.gpu_velocity()
+        pre = case.x.copy()
+        case.ex.decode_step(case.xd, case.td, case.out)
+        post, out = host(case.xd), host(case.out)
+        mism = 0
+        for b in range(w.batch):
+            z = oracle.gaussian_chunk(123 + b, 2**32 + 7, w.chunk_len, w.action_dim)
+            new, ref_out = oracle.euler_emit_shift(pre[b], case.t[b], v[b], z, np.float32)
+            assert np.array_equal(out[b], ref_out)
+            assert np.array_equal(post[b, :-1], new[:-1])
+            mism += int(np.count_nonzero(post[b, -1] != z))
+            assert np.max(np.abs(post[b, -1] - z)) <= 1e-6
+        assert mism <= 2  # fp64 libm ties only
+        assert case.ex.noise_state == (123, 2**32 + 8)
+    finally:
+        case.close()
+
+
+def test_causality_bit_exact_on_gpu():
+    """Perturbing chunks after k leaves the velocity of chunks <= k unchanged, bitwise."""
+    w = synth.workload("small_bf16")
+    case = Case(w)
+    try:
+        base = case.gpu_velocity()
+        for k in range(w.n_chunks - 1):
+            x2 = case.x.copy()
+            x2[:, k + 1:] = synth.perturbed(case.x[:, k + 1:], 9, f"gpu_causal{k}")
+            v2 = case.gpu_velocity(x2)
+            assert np.array_equal(v2[:, :k + 1], base[:, :k + 1]), k
+            assert not np.array_equal(v2[:, k + 1:], base[:, k + 1:])
+    finally:
+        case.close()
+
+
+def test_stream_isolation_and_determinism():
+    w = synth.workload("small_bf16_b3")
+    case = Case(w)
+    try:
+        v1 = case.gpu_velocity()
+        v2 = case.gpu_velocity()
+        assert np.array_equal(v1, v2)
+        x2 = case.x.copy()
+        x2[1] = synth.perturbed(case.x[1], 4, "iso")
+        v3 = case.gpu_velocity(x2)
+        assert np.array_equal(v3[0], v1[0]) and np.array_equal(v3[2], v1[2])
+        assert not np.array_equal(v3[1], v1[1])
+    finally:
+        case.close()
+
+
+def test_graph_and_eager_agree():
+    w = synth.workload("small_bf16")
+    case = Case(w)
+    try:
+        vg = case.gpu_velocity()
+        case.ex.set_graph_mode(False)
+        ve = case.gpu_velocity()
+        assert np.array_equal(vg, ve)
+    finally:
+        case.close()
+
+
+@pytest.mark.parametrize("name", ["tiny_fp32", "small_bf16"])
+def test_sequential_decode_parity(name):
+    w = synth.workload(name).replace(n_chunks=1)
+    case = Case(w)
+    try:
+        import torch
+        noise = synth.make_buffer(w, 17)[:, 0]
+        nd = dev(noise)
+        out = torch.empty_like(nd)
+        case.ex.sequential_decode(nd, 10, out)
+        got = host(out)
+        ref = oracle.sequential_decode(noise, 10, case.k, case.v, case.lens, case.W, w)
+        for b in range(w.batch):
+            assert rel_err(got[b], ref[b]) < tol(w)
+    finally:
+        case.close()
