@@ -221,6 +221,32 @@ def measure_sequential(w, chunks, warmup):
         ex.close()
 
 
+STAGE_IDS = {"film_maps": 0, "qkv_gemm": 1, "attention": 2, "gate_up_gemm": 3}
+
+
+def pmc_driver(w, stage):
+    """One velocity pass, 20 launches of one stage, then a 256 MiB copy."""
+    import torch
+    from paper_2608_27384_amd.flashvla import Expert
+    inp = Inputs(w)
+    ex = Expert(inp.W, w, w.batch, w.max_prefix)
+    try:
+        ex.set_prefix(inp.kd, inp.vd, inp.lens)
+        xd = torch.from_numpy(inp.x).cuda()
+        td = torch.from_numpy(inp.t).cuda()
+        vo = torch.empty_like(xd)
+        ex.set_graph_mode(False)
+        ex.velocity(xd, td, vo)
+        ex.debug_stage(STAGE_IDS[stage], 0, 20)
+        src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"pmc driver: {w.name} stage {stage} x20, copy 256 MiB", flush=True)
+    finally:
+        ex.close()
+
+
 # ---------------------------------------------------------------- CPU side
 
 def cpu_baseline(w, budget_s=20.0):
@@ -260,6 +286,10 @@ def main():
     ap.add_argument("--workload", default="pi05_b1")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-others", action="store_true")
+    ap.add_argument("--pmc-driver", default=None, metavar="STAGE",
+                    help="counter-run driver: one velocity pass, then 20 launches of the named "
+                         "stage (film_maps|qkv_gemm|attention|gate_up_gemm) and a 256 MiB "
+                         "device copy used to calibrate byte counters; prints no JSON")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the decode step runs on a single MI355X and "
@@ -271,6 +301,9 @@ def main():
     torch.cuda.set_device(0)
 
     w = synth.workload(args.workload)
+    if args.pmc_driver:
+        pmc_driver(w, args.pmc_driver)
+        return
     main_res = measure_streaming(w, args.steps, args.warmup, with_roofline=True)
     print(f"# {w.name}: {main_res['ms_per_step'] * 1e3:.1f} us/step, "
           f"p50 {main_res['p50_us']:.1f} us", file=sys.stderr, flush=True)
@@ -287,8 +320,12 @@ def main():
               file=sys.stderr, flush=True)
 
     stages = main_res.pop("stages")
-    dom_name = max(stages, key=lambda k: stages[k]["us"] * (
-        2 * w.n_layers if k not in ("film_maps",) else 1))
+    # dominant kernel: largest time per step (the FiLM maps run once per step,
+    # the other stages once per layer)
+    per_step = {k: v["us"] * (1 if k == "film_maps" else w.n_layers) for k, v in stages.items()}
+    for k in stages:
+        stages[k]["us_per_step"] = per_step[k]
+    dom_name = max(per_step, key=per_step.get)
     dom = stages[dom_name]
     bound = "mfma" if dom["mfma_frac"] >= dom["hbm_frac"] else "hbm"
     peak = MFMA_BF16_PEAK_TFS if w.dtype == synth.BF16 else MFMA_FP32_PEAK_TFS

@@ -1,0 +1,99 @@
+"""GPU parity at the benchmark's full sizes, in the configuration bench.py times.
+
+The oracle (fp64) computes sampled outputs: every chunk of one stream for the
+batch-1 workloads, two sampled streams of the 64-stream workload, and one
+emitted chunk of the sequential baseline.  Tolerance: max relative error 1e-2
+per (stream, chunk) slice in bf16 mode.
+"""
+import sys
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_util import Case, dev, host, rel_err, tol
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.mark.parametrize("name", ["pi05_b1", "short_chunk"])
+def test_velocity_parity_full_size(name):
+    w = synth.workload(name)
+    case = Case(w)
+    try:
+        t0 = time.time()
+        v = case.gpu_velocity()
+        ref = case.oracle_velocity(0)
+        errs = [rel_err(v[0, k], ref[k]) for k in range(w.n_chunks)]
+        _say(f"{name}: per-chunk rel err max {max(errs):.2e} ({time.time() - t0:.1f}s)")
+        assert max(errs) < tol(w), errs
+    finally:
+        case.close()
+
+
+def test_velocity_parity_batched64_sampled_streams():
+    w = synth.workload("batched64")
+    case = Case(w)
+    try:
+        v = case.gpu_velocity()
+        assert np.all(np.isfinite(v))
+        # the shortest-prefix and the longest-prefix stream
+        for b in (int(np.argmin(case.lens)), int(np.argmax(case.lens))):
+            ref = case.oracle_velocity(b)
+            errs = [rel_err(v[b, k], ref[k]) for k in range(w.n_chunks)]
+            _say(f"batched64 stream {b} (P={case.lens[b]}): max rel err {max(errs):.2e}")
+            assert max(errs) < tol(w), (b, errs)
+    finally:
+        case.close()
+
+
+def test_decode_steps_lockstep_pi05():
+    """Two steps of the headline workload: emitted chunk within tolerance of
+    the oracle, shifted slots bit-exact against the fp32 queue update of the
+    GPU's own velocity, refill equal to the oracle's Philox draw."""
+    w = synth.workload("pi05_b1")
+    case = Case(w, noise_seed=7)
+    try:
+        for s in range(2):
+            pre = host(case.xd).copy()
+            v = case.gpu_velocity(pre)
+            case.ex.decode_step(case.xd, case.td, case.out)
+            post, out = host(case.xd), host(case.out)
+            z = oracle.gaussian_chunk(7, s, w.chunk_len, w.action_dim)
+            new, ref_out = oracle.euler_emit_shift(pre[0], case.t[0], v[0], z, np.float32)
+            assert np.array_equal(out[0], ref_out)
+            assert np.array_equal(post[0, :-1], new[:-1])
+            assert np.max(np.abs(post[0, -1] - z)) <= 1e-6
+            ref_v = oracle.velocity(pre[0], case.t[0], case.k[:, 0], case.v[:, 0],
+                                    int(case.lens[0]), case.W, w)
+            _, o_out = oracle.euler_emit_shift(pre[0], case.t[0], ref_v, z)
+            err = rel_err(out[0], o_out)
+            _say(f"pi05 step {s}: emitted chunk rel err {err:.2e}")
+            assert err < tol(w)
+    finally:
+        case.close()
+
+
+def test_sequential_baseline_parity():
+    w = synth.workload("seq_baseline")
+    case = Case(w)
+    try:
+        import torch
+        noise = synth.make_buffer(w, 3)[:, 0]
+        nd = dev(noise)
+        out = torch.empty_like(nd)
+        case.ex.sequential_decode(nd, w.seq_steps, out)
+        got = host(out)
+        ref = oracle.sequential_decode(noise, w.seq_steps, case.k, case.v, case.lens, case.W, w)
+        err = rel_err(got[0], ref[0])
+        _say(f"seq_baseline: emitted chunk rel err {err:.2e}")
+        assert err < tol(w)
+    finally:
+        case.close()
