@@ -10,13 +10,14 @@
 //
 // Work split: the query rows of one (stream, kv head) are the (token, head)
 // pairs of its query-head group, flattened token-major; a block of 4 waves
-// takes 128 consecutive rows (32 per wave, as two 16-row MFMA groups that
-// share every K and V fragment read from LDS), so rows of all heads that
-// share the kv head reuse one K/V tile.  The next K/V tile is loaded into
-// registers while the current one is multiplied.  Rows of a block may straddle a chunk
+// takes 64 consecutive rows (16 per wave; RG groups of 16 rows per wave share
+// every K and V fragment read from LDS), so rows of all heads that share the
+// kv head reuse one K/V tile.  The next K/V tile is loaded into registers
+// while the current one is multiplied.  Rows of a block may straddle a chunk
 // boundary; each lane masks with its own row's limit.  Optionally the key
-// tiles of a block are split over gridDim.z blocks whose partial (o, max,
-// sum) are merged in a fixed order by attn_combine.
+// tiles of a block are split over gridDim.z blocks whose normalised partial
+// outputs (in the element type) and (max, sum) are merged in a fixed order
+// by attn_combine.
 //
 // Per key tile (KT keys): K [KT][dh] and V^T [dh][KT] are staged in LDS;
 // each wave forms S^T = K Q^T with MFMA, so a lane holds the scores of one
@@ -29,12 +30,14 @@ namespace fv {
 
 namespace {
 
-constexpr int kRowsPerWave = 32;                 // two 16-row MFMA groups
-constexpr float kSlack = 8.0f;                   // lazy softmax reference slack (log2)
-constexpr int kRowsPerBlock = 4 * kRowsPerWave;
+constexpr float kSlack = 8.0f;  // lazy softmax reference slack (log2 units)
+constexpr int kRG = 1;          // 16-row MFMA groups per wave
+constexpr int kRowsPerBlock = 4 * 16 * kRG;
 
-template <typename T, int DH, int KT>
+template <typename T, int DH, int KT, int RG>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
+  constexpr int kRowsPerWave = 16 * RG;
+  constexpr int kRowsPerBlock = 4 * kRowsPerWave;
   using MF = Mfma<T>;
   constexpr int EPV = 16 / (int)sizeof(T);
   constexpr int LDK = DH + EPV;
@@ -61,10 +64,10 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int l16 = lane & 15, lg = lane >> 4;
 
   // this lane's two query rows (one per 16-row group)
-  int tok[2], head[2], lim[2];
-  bool valid[2];
+  int tok[RG], head[RG], lim[RG];
+  bool valid[RG];
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
+  for (int q = 0; q < RG; ++q) {
     const int rq = tile0 + kRowsPerWave * wave + 16 * q + l16;
     valid[q] = rq < rows_bg;
     const int rqc = valid[q] ? rq : rows_bg - 1;
@@ -77,21 +80,24 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int nkt = (lim_max + KT - 1) / KT;
   const int kt_begin = (split * nkt) / a.n_split, kt_end = ((split + 1) * nkt) / a.n_split;
 
-  typename MF::frag qf[2][NKS];
+  typename MF::frag qf[RG][NKS];
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
+  for (int q = 0; q < RG; ++q) {
     const T* qrow = reinterpret_cast<const T*>(a.q) +
                     ((size_t)(b * a.tokens + tok[q]) * a.n_q_heads + head[q]) * DH;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) qf[q][ks] = MF::load(qrow + ks * MF::KM + MF::KG * lg);
   }
 
-  f32x4 acc[2][NDT];
+  f32x4 acc[RG][NDT];
+  float m_run[RG], l_run[RG];
 #pragma unroll
-  for (int q = 0; q < 2; ++q)
+  for (int q = 0; q < RG; ++q) {
+    m_run[q] = -INFINITY;
+    l_run[q] = 0.f;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) acc[q][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+  }
 
   const T* kbase = reinterpret_cast<const T*>(a.karena) +
                    ((size_t)b * a.n_kv_heads + g) * (size_t)a.S * DH;
@@ -149,18 +155,18 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     __syncthreads();
     load_tile(min(kt + 1, kt_clamp));  // overlaps the MFMA work below
 
-    // S^T = K Q^T for both row groups; K fragments are shared
-    f32x4 s[2][NST];
+    // S^T = K Q^T for every row group; K fragments are shared
+    f32x4 s[RG][NST];
 #pragma unroll
     for (int st = 0; st < NST; ++st) {
-      s[0][st] = f32x4{0.f, 0.f, 0.f, 0.f};
-      s[1][st] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int q = 0; q < RG; ++q) s[q][st] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
         const typename MF::frag kf =
             MF::load(&sK[(16 * st + l16) * LDK + ks * MF::KM + MF::KG * lg]);
-        s[0][st] = MF::mma(kf, qf[0][ks], s[0][st]);
-        s[1][st] = MF::mma(kf, qf[1][ks], s[1][st]);
+#pragma unroll
+        for (int q = 0; q < RG; ++q) s[q][st] = MF::mma(kf, qf[q][ks], s[q][st]);
       }
     }
     // Online softmax per query row (a lane owns one row of each group) with
@@ -169,9 +175,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     // (log2 units), so probabilities stay below 2^kSlack and the costly
     // rescale of the accumulators runs only when some row of the wave moved.
     bool moved = false;
-    float alpha[2];
+    float alpha[RG];
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < RG; ++q) {
       float mt = -INFINITY;
 #pragma unroll
       for (int st = 0; st < NST; ++st)
@@ -206,9 +212,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       l_run[q] = l_run[q] * alpha[q] + ls;
       m_run[q] = m_new;
     }
-    if (__builtin_amdgcn_read_exec() && __any(moved)) {
+    if (__any(moved)) {
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
+      for (int q = 0; q < RG; ++q)
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) acc[q][dt] *= alpha[q];
     }
@@ -217,9 +223,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     if constexpr (kBF16) {
 #pragma unroll
       for (int kc = 0; kc < NST / 2; ++kc) {
-        bf16x8 pf[2];
+        bf16x8 pf[RG];
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
+        for (int q = 0; q < RG; ++q) {
           u16x8 pb;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
@@ -235,8 +241,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
           const u16x4 hi = *reinterpret_cast<const u16x4*>(vr + 16);
           const bf16x8 vf = __builtin_bit_cast(
               bf16x8, u16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
-          acc[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[0], acc[0][dt], 0, 0, 0);
-          acc[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[1], acc[1][dt], 0, 0, 0);
+#pragma unroll
+          for (int q = 0; q < RG; ++q)
+            acc[q][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[q], acc[q][dt], 0, 0, 0);
         }
       }
     } else {
@@ -247,66 +254,85 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
           for (int dt = 0; dt < NDT; ++dt) {
             const float vf = (float)sV[(16 * dt + l16) * LDV + 16 * st + 4 * lg + r];
-            acc[0][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, (float)s[0][st][r], acc[0][dt],
-                                                              0, 0, 0);
-            acc[1][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, (float)s[1][st][r], acc[1][dt],
-                                                              0, 0, 0);
+#pragma unroll
+            for (int q = 0; q < RG; ++q)
+              acc[q][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, (float)s[q][st][r], acc[q][dt],
+                                                                0, 0, 0);
           }
     }
   }
 
   const size_t R = (size_t)a.B * a.tokens * a.n_q_heads;
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
+  for (int q = 0; q < RG; ++q) {
     if (!valid[q]) continue;
     const size_t grow = (size_t)(b * a.tokens + tok[q]) * a.n_q_heads + head[q];
-    if (a.n_split == 1) {
-      const float inv = 1.0f / l_run[q];
-      T* orow = reinterpret_cast<T*>(a.o) + grow * DH;
+    // normalised output (a split with no visible key stores zeros)
+    const float inv = l_run[q] > 0.f ? 1.0f / l_run[q] : 0.f;
+    T* orow = a.n_split == 1
+                  ? reinterpret_cast<T*>(a.o) + grow * DH
+                  : reinterpret_cast<T*>(a.part_o) + ((size_t)split * R + grow) * DH;
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
+    for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) orow[16 * dt + 4 * lg + r] = from_f32<T>(acc[q][dt][r] * inv);
-    } else {
-      float* po = a.part_o + ((size_t)split * R + grow) * DH;
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) *reinterpret_cast<f32x4*>(po + 16 * dt + 4 * lg) = acc[q][dt];
-      if (lg == 0) {
-        a.part_ml[((size_t)split * R + grow) * 2 + 0] = m_run[q];
-        a.part_ml[((size_t)split * R + grow) * 2 + 1] = l_run[q];
-      }
+      for (int r = 0; r < 4; ++r) orow[16 * dt + 4 * lg + r] = from_f32<T>(acc[q][dt][r] * inv);
+    if (a.n_split > 1 && lg == 0) {
+      a.part_ml[((size_t)split * R + grow) * 2 + 0] = m_run[q];
+      a.part_ml[((size_t)split * R + grow) * 2 + 1] = l_run[q];
     }
   }
 }
 
-// Merge of split partials in split order: o = sum_z 2^(m_z - M) o_z / sum_z 2^(m_z - M) l_z.
-// One wave per row; a lane owns 4 consecutive features.
+// Merge of split partials in split order.  Partial z holds o_z = acc_z / l_z
+// (stored in the element type) with its reference m_z and sum l_z:
+// o = sum_z 2^(m_z - M) l_z o_z / sum_z 2^(m_z - M) l_z.  One wave per row; a
+// lane owns 4 consecutive features.
 template <typename T, int DH>
-__global__ __launch_bounds__(256) void attn_combine(const float* __restrict__ part_o,
+__global__ __launch_bounds__(256) void attn_combine(const T* __restrict__ part_o,
                                                     const float* __restrict__ part_ml,
                                                     T* __restrict__ o, int R, int n_split) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= R) return;
-  float M = -INFINITY;
+  // every load of the row is issued before any is used (n_split <= 8)
   float mz[8], lz[8];
-  for (int z = 0; z < n_split; ++z) {
-    mz[z] = part_ml[((size_t)z * R + row) * 2];
-    lz[z] = part_ml[((size_t)z * R + row) * 2 + 1];
-    M = fmaxf(M, mz[z]);
+#pragma unroll
+  for (int z = 0; z < 8; ++z) {
+    mz[z] = z < n_split ? part_ml[((size_t)z * R + row) * 2] : -INFINITY;
+    lz[z] = z < n_split ? part_ml[((size_t)z * R + row) * 2 + 1] : 0.f;
   }
+  constexpr int NV = (DH + 255) / 256;  // 4-feature groups per lane
+  float pv[8][NV][4];
+#pragma unroll
+  for (int z = 0; z < 8; ++z)
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int d = 4 * lane + 256 * v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        pv[z][v][i] = (z < n_split && d < DH) ? to_f32(part_o[((size_t)z * R + row) * DH + d + i]) : 0.f;
+    }
+  float M = -INFINITY;
+#pragma unroll
+  for (int z = 0; z < 8; ++z) M = fmaxf(M, mz[z]);
   float den = 0.f;
-  for (int z = 0; z < n_split; ++z) {
-    mz[z] = exp2f(mz[z] - M);
-    den += mz[z] * lz[z];
+#pragma unroll
+  for (int z = 0; z < 8; ++z) {
+    mz[z] = lz[z] > 0.f ? exp2f(mz[z] - M) * lz[z] : 0.f;  // weight of split z
+    den += mz[z];
   }
   const float inv = 1.0f / den;
-  for (int d = 4 * lane; d < DH; d += 256) {
-    f32x4 num = {0.f, 0.f, 0.f, 0.f};
-    for (int z = 0; z < n_split; ++z)
-      num += mz[z] * *reinterpret_cast<const f32x4*>(part_o + ((size_t)z * R + row) * DH + d);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) o[(size_t)row * DH + d + i] = from_f32<T>(num[i] * inv);
+  for (int v = 0; v < NV; ++v) {
+    const int d = 4 * lane + 256 * v;
+    if (d >= DH) continue;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float num = 0.f;
+#pragma unroll
+      for (int z = 0; z < 8; ++z) num += mz[z] * pv[z][v][i];
+      o[(size_t)row * DH + d + i] = from_f32<T>(num * inv);
+    }
   }
 }
 
@@ -316,10 +342,11 @@ void launch_dh(const AttnArgs& a, hipStream_t s) {
   constexpr int KT = (sizeof(T) == 2 && DH < 192) ? 64 : 32;
   const int G = a.n_q_heads / a.n_kv_heads;
   dim3 grid((a.tokens * G + kRowsPerBlock - 1) / kRowsPerBlock, a.B * a.n_kv_heads, a.n_split);
-  hipLaunchKernelGGL((attn_kernel<T, DH, KT>), grid, dim3(256), 0, s, a);
+  hipLaunchKernelGGL((attn_kernel<T, DH, KT, kRG>), grid, dim3(256), 0, s, a);
   if (a.n_split > 1) {
     const int R = a.B * a.tokens * a.n_q_heads;
-    hipLaunchKernelGGL((attn_combine<T, DH>), dim3((R + 3) / 4), dim3(256), 0, s, a.part_o, a.part_ml,
+    hipLaunchKernelGGL((attn_combine<T, DH>), dim3((R + 3) / 4), dim3(256), 0, s,
+                       reinterpret_cast<const T*>(a.part_o), a.part_ml,
                        reinterpret_cast<T*>(a.o), R, a.n_split);
   }
 }

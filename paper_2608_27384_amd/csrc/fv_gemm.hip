@@ -291,38 +291,53 @@ struct EpiQkv {
     static_assert(FN % 2 == 0, "QKV epilogue needs column pairs");
     const int dh = a.head_dim, half = dh / 2;
     const int qd = a.n_q_heads * dh, kd = a.n_kv_heads * dh;
+    const int2* __restrict__ row_pos = a.row_pos;
+    const float* __restrict__ rcos = a.rcos;
+    const float* __restrict__ rsin = a.rsin;
 #pragma unroll
-    for (int j = 0; j < FN; j += 2) {
-      const int c0 = col0 + 32 * j;  // first packed column of the pair group
+    for (int i = 0; i < FM; ++i) {
+      // all row lookups of this 32-row slab first (they are independent)
+      int2 rp[16];
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+      for (int r = 0; r < 16; ++r) rp[r] = row_pos[min(row0 + 32 * i + acc_row(r, lane), M - 1)];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = row0 + 32 * i + acc_row(r, lane);
-          if (row >= M) continue;
-          const int2 rp = a.row_pos[row];  // (stream, arena row)
-          const int b = rp.x, pos = rp.y;
-          const float x0 = acc[i][j][r], x1 = acc[i][j + 1][r];
-          if (c0 < qd + kd) {
-            const bool isq = c0 < qd;
-            const int cc = isq ? c0 : c0 - qd;
-            const int head = cc / dh;
-            const int dlo = 32 * ((cc - head * dh) >> 6) + (lane & 31), dhi = dlo + half;
-            const float cs = a.rcos[(size_t)pos * half + dlo];
-            const float sn = a.rsin[(size_t)pos * half + dlo];
-            const float y0 = x0 * cs - x1 * sn, y1 = x1 * cs + x0 * sn;
+      for (int j = 0; j < FN; j += 2) {
+        const int c0 = col0 + 32 * j;  // first packed column of the pair group
+        if (c0 < qd + kd) {
+          const bool isq = c0 < qd;
+          const int cc = isq ? c0 : c0 - qd;
+          const int head = cc / dh;
+          const int dlo = 32 * ((cc - head * dh) >> 6) + (lane & 31), dhi = dlo + half;
+          float cs[16], sn[16];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            cs[r] = rcos[(size_t)rp[r].y * half + dlo];
+            sn[r] = rsin[(size_t)rp[r].y * half + dlo];
+          }
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = row0 + 32 * i + acc_row(r, lane);
+            if (row >= M) continue;
+            const float x0 = acc[i][j][r], x1 = acc[i][j + 1][r];
+            const float y0 = x0 * cs[r] - x1 * sn[r], y1 = x1 * cs[r] + x0 * sn[r];
             T* dst = isq ? a.q + (size_t)row * qd + head * dh
-                         : a.karena + (((size_t)b * a.n_kv_heads + head) * a.S + pos) * dh;
+                         : a.karena + (((size_t)rp[r].x * a.n_kv_heads + head) * a.S + rp[r].y) * dh;
             dst[dlo] = from_f32<T>(y0);
             dst[dhi] = from_f32<T>(y1);
-          } else {
-            const int cc = c0 - qd - kd;
-            const int g = cc / dh, d = cc - g * dh + (lane & 31);
-            T* base = a.vtarena + ((size_t)b * a.n_kv_heads + g) * dh * a.S + pos;
-            base[(size_t)d * a.S] = from_f32<T>(x0);
-            base[(size_t)(d + 32) * a.S] = from_f32<T>(x1);
+          }
+        } else {
+          const int cc = c0 - qd - kd;
+          const int g = cc / dh, d = cc - g * dh + (lane & 31);
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = row0 + 32 * i + acc_row(r, lane);
+            if (row >= M) continue;
+            T* base = a.vtarena + ((size_t)rp[r].x * a.n_kv_heads + g) * dh * a.S + rp[r].y;
+            base[(size_t)d * a.S] = from_f32<T>(acc[i][j][r]);
+            base[(size_t)(d + 32) * a.S] = from_f32<T>(acc[i][j + 1][r]);
           }
         }
+      }
     }
   }
 };
@@ -331,18 +346,24 @@ struct EpiGatedResid {
   float* h; const float* mod; int mod_ld, gate_off, chunk_len, ldh;
   template <int FM, int FN>
   __device__ void apply(f32x16 (&acc)[FM][FN], int row0, int col0, int lane, int M) const {
+    float* __restrict__ hh = h;
+    const float* __restrict__ mm = mod;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = row0 + 32 * i + acc_row(r, lane);
-        if (row >= M) continue;
-        const float* g = mod + (size_t)(row / chunk_len) * mod_ld + gate_off;
+      for (int j = 0; j < FN; ++j) {
+        const int col = col0 + 32 * j + (lane & 31);
+        float hv[16], gv[16];
 #pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const int col = col0 + 32 * j + (lane & 31);
-          float* hp = h + (size_t)row * ldh + col;
-          *hp = *hp + g[col] * acc[i][j][r];
+        for (int r = 0; r < 16; ++r) {  // independent loads first
+          const int row = min(row0 + 32 * i + acc_row(r, lane), M - 1);
+          hv[r] = hh[(size_t)row * ldh + col];
+          gv[r] = mm[(size_t)(row / chunk_len) * mod_ld + gate_off + col];
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = row0 + 32 * i + acc_row(r, lane);
+          if (row < M) hh[(size_t)row * ldh + col] = hv[r] + gv[r] * acc[i][j][r];
         }
       }
   }

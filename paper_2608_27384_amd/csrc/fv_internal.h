@@ -158,7 +158,7 @@ struct AttnArgs {
   const void* vtarena;  // layer base [Bmax][Hkv][dh][S]
   const int* len;
   void* o;              // [B*tokens][Hq*dh]
-  float* part_o;        // [n_split][B*tokens*Hq][dh]
+  void* part_o;         // [n_split][B*tokens*Hq][dh] element type, normalised
   float* part_ml;       // [n_split][B*tokens*Hq][2]
   int B, tokens, chunk_len, n_q_heads, n_kv_heads, head_dim, S, n_split;
 };
@@ -212,7 +212,7 @@ struct Handle {
   void* m = nullptr;                                              // T [Bmax*T][F]
   float* v = nullptr;                                             // [Bmax][K][C][A]
   int2* row_pos = nullptr;                                        // [Bmax*T]
-  float* part_o = nullptr; float* part_ml = nullptr; int max_split = 1;
+  void* part_o = nullptr; float* part_ml = nullptr; int max_split = 1;
   float* seq_x = nullptr; float* seq_t = nullptr;
   std::vector<std::pair<int, float*>> tscheds;  // sequential-decode t_j tables by step count
 

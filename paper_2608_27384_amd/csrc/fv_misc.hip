@@ -81,6 +81,7 @@ __global__ __launch_bounds__(256) void embed_adarms_kernel(
     const f32x4 bias = *reinterpret_cast<const f32x4*>(b_in + c);
 #pragma unroll
     for (int r = 0; r < kEmbRows; ++r) acc[r] = bias;
+#pragma unroll 8
     for (int a = 0; a < A; ++a) {
       const f32x4 wv = *reinterpret_cast<const f32x4*>(w_in + (size_t)a * W + c);
 #pragma unroll
@@ -139,11 +140,17 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const float* __restrict
   for (int q = 0; q < 2; ++q) {
     const int c = 4 * tid + 1024 * q;
     if (c < W) {
-      f32x4 acc = *reinterpret_cast<const f32x4*>(part + (size_t)row * W + c);
-      for (int z = 1; z < ks; ++z)
-        acc += *reinterpret_cast<const f32x4*>(part + ((size_t)z * rows + row) * W + c);
+      f32x4 pz[8];  // every split's load issued before the sum (ks <= 8)
+#pragma unroll
+      for (int z = 0; z < 8; ++z)
+        pz[z] = z < ks ? *reinterpret_cast<const f32x4*>(part + ((size_t)z * rows + row) * W + c)
+                       : f32x4{0.f, 0.f, 0.f, 0.f};
       const f32x4 g = *reinterpret_cast<const f32x4*>(mrow + gate_off + c);
       f32x4 hv = *reinterpret_cast<const f32x4*>(h + (size_t)row * W + c);
+      f32x4 acc = pz[0];
+#pragma unroll
+      for (int z = 1; z < 8; ++z)
+        if (z < ks) acc += pz[z];
       hv += g * acc;
       *reinterpret_cast<f32x4*>(h + (size_t)row * W + c) = hv;
       hq[q] = hv;
@@ -185,36 +192,44 @@ __global__ __launch_bounds__(256) void adarms_kernel(const float* __restrict__ h
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= rows) return;
+  constexpr int NV = 2048 / 256;  // 4-float groups per lane for W <= 2048
   const float* hr = h + (size_t)row * W;
-  float ss = 0.f;
-  for (int c = lane * 4; c < W; c += 256) {
-    const float4 x = *reinterpret_cast<const float4*>(hr + c);
-    ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+  const float* sc = mod + (size_t)(row / chunk_len) * mod_ld + scale_off;
+  f32x4 x[NV], sv[NV], bv[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {  // all loads of the row first
+    const int c = 4 * lane + 256 * i;
+    const bool ok = c < W;
+    x[i] = ok ? *reinterpret_cast<const f32x4*>(hr + c) : f32x4{0.f, 0.f, 0.f, 0.f};
+    sv[i] = ok ? *reinterpret_cast<const f32x4*>(sc + c) : f32x4{0.f, 0.f, 0.f, 0.f};
+    bv[i] = ok ? *reinterpret_cast<const f32x4*>(sc + W + c) : f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) ss += x[i][0] * x[i][0] + x[i][1] * x[i][1] + x[i][2] * x[i][2] + x[i][3] * x[i][3];
   ss = wave_sum(ss);
   const float rinv = 1.0f / sqrtf(ss / (float)W + eps);
-  const float* sc = mod + (size_t)(row / chunk_len) * mod_ld + scale_off;
-  const float* sh = sc + W;
   T* ur = u + (size_t)row * W;
-  for (int c = lane * 4; c < W; c += 256) {
-    const float4 x = *reinterpret_cast<const float4*>(hr + c);
-    const float4 s = *reinterpret_cast<const float4*>(sc + c);
-    const float4 b = *reinterpret_cast<const float4*>(sh + c);
-    ur[c + 0] = from_f32<T>(x.x * rinv * (1.0f + s.x) + b.x);
-    ur[c + 1] = from_f32<T>(x.y * rinv * (1.0f + s.y) + b.y);
-    ur[c + 2] = from_f32<T>(x.z * rinv * (1.0f + s.z) + b.z);
-    ur[c + 3] = from_f32<T>(x.w * rinv * (1.0f + s.w) + b.w);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = 4 * lane + 256 * i;
+    if (c < W)
+      store4<T>(ur + c, x[i][0] * rinv * (1.0f + sv[i][0]) + bv[i][0],
+                x[i][1] * rinv * (1.0f + sv[i][1]) + bv[i][1],
+                x[i][2] * rinv * (1.0f + sv[i][2]) + bv[i][2],
+                x[i][3] * rinv * (1.0f + sv[i][3]) + bv[i][3]);
   }
 }
 
 // ------------------------------------- final FiLM RMSNorm + velocity head
 // v[row] = (rmsnorm(h) (1 + scale) + shift) w_out + b_out, fp32.  A block
-// handles kFinalRows rows: each wave normalises one row into LDS.  w_out is
-// then staged through LDS 128 rows at a time; each output (row, a) is summed
-// by `parts` threads over interleaved slices of every chunk, and the slices
-// are added in a fixed order.
+// handles kFinalRows rows: each wave normalises one row into LDS (every load
+// of the row issued before use).  Then each output (row, a) is summed by
+// `parts` threads over interleaved slices of the width, reading w_out in
+// unrolled batches of independent loads, and the slices are added in a
+// fixed order.
 constexpr int kFinalRows = 4;
-constexpr int kFinalChunk = 128;
+constexpr int kMaxW = 2048;
 __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ h,
                                                     const float* __restrict__ mod, int mod_ld,
                                                     int scale_off, int chunk_len, float eps,
@@ -222,49 +237,59 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ h,
                                                     const float* __restrict__ b_out,
                                                     float* __restrict__ v, int rows, int W,
                                                     int A) {
-  extern __shared__ float smem[];  // su [kFinalRows][W], sw [kFinalChunk][A], sp [256]
+  extern __shared__ float smem[];  // su [kFinalRows][W], sp [256]
   float* su = smem;
-  float* sw = su + kFinalRows * W;
-  float* sp = sw + kFinalChunk * A;
+  float* sp = su + kFinalRows * W;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, tid = threadIdx.x;
   const int row0 = blockIdx.x * kFinalRows;
   {
-    const int row = row0 + wave;
-    if (row < rows) {
-      const float* hr = h + (size_t)row * W;
-      float ss = 0.f;
-      for (int c = lane; c < W; c += 64) ss += hr[c] * hr[c];
-      ss = wave_sum(ss);
-      const float rinv = 1.0f / sqrtf(ss / (float)W + eps);
-      const float* sc = mod + (size_t)(row / chunk_len) * mod_ld + scale_off;
-      for (int c = lane; c < W; c += 64)
-        su[wave * W + c] = hr[c] * rinv * (1.0f + sc[c]) + sc[W + c];
-    } else {
-      for (int c = lane; c < W; c += 64) su[wave * W + c] = 0.f;
+    const int row = min(row0 + wave, rows - 1);
+    const float* hr = h + (size_t)row * W;
+    const float* sc = mod + (size_t)(row / chunk_len) * mod_ld + scale_off;
+    constexpr int NPL = kMaxW / 64;
+    float hv[NPL], sv[NPL], bv[NPL];
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) {
+      const int c = lane + 64 * i;
+      hv[i] = c < W ? hr[c] : 0.f;
+      sv[i] = c < W ? sc[c] : 0.f;
+      bv[i] = c < W ? sc[W + c] : 0.f;
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) ss += hv[i] * hv[i];
+    ss = wave_sum(ss);
+    const float rinv = 1.0f / sqrtf(ss / (float)W + eps);
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) {
+      const int c = lane + 64 * i;
+      if (c < W) su[wave * W + c] = hv[i] * rinv * (1.0f + sv[i]) + bv[i];
     }
   }
+  __syncthreads();
   const int nout = kFinalRows * A;  // <= 256
   const int parts = 256 / nout;
   const int o = tid % nout, part = tid / nout;
   const int r = o / A, a = o - r * A;
-  float acc4[4] = {0.f, 0.f, 0.f, 0.f};  // independent chains keep LDS loads in flight
-  for (int n0 = 0; n0 < W; n0 += kFinalChunk) {
-    __syncthreads();
-    for (int i = tid; i < kFinalChunk * A; i += 256) sw[i] = w_out[(size_t)n0 * A + i];
-    __syncthreads();
-    if (part < parts) {
-      const float* ur = su + r * W + n0;
-#pragma unroll 8
-      for (int nn = part; nn < kFinalChunk; nn += parts)
-        acc4[nn & 3] = fmaf(ur[nn], sw[nn * A + a], acc4[nn & 3]);
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (part < parts) {
+    const float* ur = su + r * W;
+    int n = part;
+    for (; n + 7 * parts < W; n += 8 * parts) {
+      float wv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) wv[u] = w_out[(size_t)(n + u * parts) * A + a];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc[u] = fmaf(ur[n + u * parts], wv[u], acc[u]);
     }
+    for (; n < W; n += parts) acc[0] = fmaf(ur[n], w_out[(size_t)n * A + a], acc[0]);
   }
-  sp[tid] = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
+  sp[tid] = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
   __syncthreads();
-  if (tid < nout) {
+  if (tid < nout && row0 + r < rows) {
     float tot = b_out[a];
     for (int p = 0; p < parts; ++p) tot += sp[p * nout + tid];
-    if (row0 + r < rows) v[(size_t)(row0 + r) * A + a] = tot;
+    v[(size_t)(row0 + r) * A + a] = tot;
   }
 }
 
@@ -466,7 +491,7 @@ void launch_adarms(const float* h, const float* mod, int mod_ld, int scale_off, 
 void launch_final(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
                   float eps, const float* w_out, const float* b_out, float* v, int rows, int W,
                   int A, hipStream_t s) {
-  const size_t lds = (size_t)(kFinalRows * W + kFinalChunk * A + 256) * sizeof(float);
+  const size_t lds = (size_t)(kFinalRows * W + 256) * sizeof(float);
   hipLaunchKernelGGL(final_kernel, dim3((rows + kFinalRows - 1) / kFinalRows), dim3(256), lds, s, h, mod, mod_ld,
                      scale_off, chunk_len, eps, w_out, b_out, v, rows, W, A);
 }

@@ -147,9 +147,11 @@ void validate_cfg(const fv_cfg& c) {
   if (!(c.rope_theta > 0.f) || !std::isfinite(c.rope_theta)) bad("rope_theta must be > 0");
 }
 
+// Key splits per attention row tile: enough blocks for two per CU (about 512),
+// at most 8 splits.
 int attn_split(const Handle* h, int B) {
   const int base = attention_row_tiles<float>(h->T, h->Hq, h->Hkv) * B * h->Hkv;
-  int s = (256 + base - 1) / base;
+  int s = (512 + base - 1) / base;
   return s < 1 ? 1 : (s > 8 ? 8 : s);
 }
 
@@ -511,7 +513,7 @@ fv_status fv_create(const fv_weights* w, const fv_cfg* cfg, fv_handle* out) {
       const int s = attn_split(h, B);
       if (s > 1) part_rows = std::max(part_rows, (size_t)s * B * H.T * H.Hq);
     }
-    H.part_o = static_cast<float*>(dalloc(h, part_rows * dh * 4));
+    H.part_o = dalloc(h, part_rows * dh * H.esz);
     H.part_ml = static_cast<float*>(dalloc(h, part_rows * 2 * 4));
     {
       size_t ws = 0;
