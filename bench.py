@@ -34,6 +34,7 @@ import synth  # noqa: E402
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFS = 2500.0     # dense bf16 MFMA, TFLOP/s
 MFMA_FP32_PEAK_TFS = 157.3
+METRIC = "action chunks/s + p50 decode-step latency (\u00b5s), \u03c00.5-shaped, batch 1 and 64"
 
 
 # ---------------------------------------------------------------- accounting
@@ -171,26 +172,68 @@ def measure_streaming(w, steps, warmup, with_roofline):
         ex.close()
 
 
-def stage_rooflines(ex, w, lens):
-    """Per-launch algorithmic work and live-timed duration of the big stages."""
+# Timed stages: (debug-stage id, launches per step, kernel(s) it launches).
+STAGES = {
+    "film_maps": (0, "step", "gemm_kernel<..., EpiBiasF32> (all FiLM maps, one GEMM)"),
+    "qkv_gemm": (1, "layer", "gemm_kernel<..., EpiQkv> (QKV + rotary + K/V arena write)"),
+    "attention": (4, "layer", "attn_kernel (chunk-causal + prefix attention, per-split partials)"),
+    "attn_combine": (5, "layer", "attn_combine (merge of the key splits)"),
+    "o_proj": (6, "layer", "split-K gemm_kernel + resid_norm_kernel (O proj, gated residual, FiLM norm)"),
+    "gate_up_gemm": (3, "layer", "gemm_kernel<..., EpiGeglu> (gate/up + GeGLU)"),
+    "down_proj": (7, "layer", "split-K gemm_kernel + resid_norm_kernel (down proj, gated residual, FiLM norm)"),
+}
+# stages that are one kernel launch each (eligible for the roofline record)
+SINGLE_KERNEL = {"film_maps": "gemm_kernel", "qkv_gemm": "gemm_kernel",
+                 "attention": "attn_kernel", "attn_combine": "attn_combine",
+                 "gate_up_gemm": "gemm_kernel"}
+
+
+def stage_work(w, lens, n_split):
+    """Algorithmic (flops, bytes) of one launch of each timed stage.
+
+    Bytes count each operand once: weights, the activations a stage reads
+    and the results it writes; for attention the queries, the visible keys
+    and values (valid prefix + the buffer's own tokens) and the output.  The
+    split partials of the attention are an implementation choice and count
+    only for the combine stage, whose whole job they are."""
     e = 2 if w.dtype == synth.BF16 else 4
     W, F = w.width, w.mlp_dim
     qd, kd = w.n_q_heads * w.head_dim, w.n_kv_heads * w.head_dim
     ngu = 2 * F if w.mlp_gated else F
     rows_t, rows_k = w.batch * w.tokens, w.batch * w.n_chunks
     nmod = (6 * w.n_layers + 2) * W
-    peak = MFMA_BF16_PEAK_TFS if w.dtype == synth.BF16 else MFMA_FP32_PEAK_TFS
-    out = {}
-    specs = {
-        "film_maps": (0, 2 * rows_k * W * nmod, nmod * W * e + nmod * 4),
-        "qkv_gemm": (1, 2 * rows_t * W * (qd + 2 * kd), W * (qd + 2 * kd) * e),
-        "attention": (2, sum(4 * w.head_dim * w.n_q_heads * visible_pairs(w, p) for p in lens),
-                      2 * int(np.sum(lens)) * kd * e),
-        "gate_up_gemm": (3, 2 * rows_t * W * ngu, W * ngu * e),
+    kv_bytes = 2 * (int(np.sum(lens)) + rows_t) * kd * e
+    R = rows_t * w.n_q_heads
+    comb_bytes = (n_split * R * (w.head_dim * e + 8) + R * w.head_dim * e) if n_split > 1 else 0
+    return {
+        "film_maps": (2 * rows_k * W * nmod, nmod * W * e + nmod * 4 + rows_k * (W * e + nmod * 4)),
+        "qkv_gemm": (2 * rows_t * W * (qd + 2 * kd), W * (qd + 2 * kd) * e + rows_t * W * e
+                     + rows_t * (qd + 2 * kd) * e),
+        "attention": (sum(4 * w.head_dim * w.n_q_heads * visible_pairs(w, p) for p in lens),
+                      rows_t * qd * e + kv_bytes + rows_t * qd * e),
+        "attn_combine": (0, comb_bytes),
+        "o_proj": (2 * rows_t * qd * W, qd * W * e + rows_t * qd * e + 2 * rows_t * W * 4
+                   + rows_t * W * e),
+        "gate_up_gemm": (2 * rows_t * W * ngu, W * ngu * e + rows_t * W * e + rows_t * F * e),
+        "down_proj": (2 * rows_t * F * W, F * W * e + rows_t * F * e + 2 * rows_t * W * 4
+                      + rows_t * W * e),
     }
-    for name, (stage, flops, nbytes) in specs.items():
+
+
+def stage_rooflines(ex, w, lens):
+    """Per-launch algorithmic work and live-timed (HIP events) duration of each stage."""
+    peak = MFMA_BF16_PEAK_TFS if w.dtype == synth.BF16 else MFMA_FP32_PEAK_TFS
+    work = stage_work(w, lens, ex.attn_split())
+    out = {}
+    for name, (stage, per, kern) in STAGES.items():
+        flops, nbytes = work[name]
+        if nbytes == 0:
+            continue
         ms = time_stage(ex, stage, 0)
-        out[name] = {"us": ms * 1e3, "tflops": flops / (ms / 1e3) / 1e12,
+        n = 1 if per == "step" else w.n_layers
+        out[name] = {"us": ms * 1e3, "launches_per_step": n, "us_per_step": ms * 1e3 * n,
+                     "kernels": kern,
+                     "tflops": flops / (ms / 1e3) / 1e12,
                      "gbs": nbytes / (ms / 1e3) / 1e9,
                      "mfma_frac": flops / (ms / 1e3) / (peak * 1e12),
                      "hbm_frac": nbytes / (ms / 1e3) / (HBM_PEAK_GBS * 1e9),
@@ -221,9 +264,6 @@ def measure_sequential(w, chunks, warmup):
         ex.close()
 
 
-STAGE_IDS = {"film_maps": 0, "qkv_gemm": 1, "attention": 2, "gate_up_gemm": 3}
-
-
 def pmc_driver(w, stage):
     """One velocity pass, 20 launches of one stage, then a 256 MiB copy."""
     import torch
@@ -237,7 +277,7 @@ def pmc_driver(w, stage):
         vo = torch.empty_like(xd)
         ex.set_graph_mode(False)
         ex.velocity(xd, td, vo)
-        ex.debug_stage(STAGE_IDS[stage], 0, 20)
+        ex.debug_stage(STAGES[stage][0], 0, 20)
         src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         dst.copy_(src)
@@ -288,7 +328,7 @@ def main():
     ap.add_argument("--no-others", action="store_true")
     ap.add_argument("--pmc-driver", default=None, metavar="STAGE",
                     help="counter-run driver: one velocity pass, then 20 launches of the named "
-                         "stage (film_maps|qkv_gemm|attention|gate_up_gemm) and a 256 MiB "
+                         "stage (one of " + "|".join(STAGES) + ") and a 256 MiB "
                          "device copy used to calibrate byte counters; prints no JSON")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -320,21 +360,24 @@ def main():
               file=sys.stderr, flush=True)
 
     stages = main_res.pop("stages")
-    # dominant kernel: largest time per step (the FiLM maps run once per step,
-    # the other stages once per layer)
-    per_step = {k: v["us"] * (1 if k == "film_maps" else w.n_layers) for k, v in stages.items()}
-    for k in stages:
-        stages[k]["us_per_step"] = per_step[k]
-    dom_name = max(per_step, key=per_step.get)
+    # dominant kernel: the single-kernel stage with the largest time per step
+    dom_name = max((k for k in stages if k in SINGLE_KERNEL),
+                   key=lambda k: stages[k]["us_per_step"])
     dom = stages[dom_name]
     bound = "mfma" if dom["mfma_frac"] >= dom["hbm_frac"] else "hbm"
     peak = MFMA_BF16_PEAK_TFS if w.dtype == synth.BF16 else MFMA_FP32_PEAK_TFS
-    roofline = {"kernel": dom_name, "bound": bound,
+    from paper_2608_27384_amd import counters
+    tr = counters.load_traffic(dom_name, w.name)
+    roofline = {"bound": bound,
                 "achieved": dom["tflops"] if bound == "mfma" else dom["gbs"],
                 "peak": peak if bound == "mfma" else HBM_PEAK_GBS,
                 "unit": "TFLOP/s" if bound == "mfma" else "GB/s",
                 "frac": dom["mfma_frac"] if bound == "mfma" else dom["hbm_frac"],
-                "traffic": None, "us_per_launch": dom["us"]}
+                "traffic": tr["bytes"] if tr else None,
+                "kernel": SINGLE_KERNEL[dom_name], "stage": dom_name,
+                "us_per_launch": dom["us"], "launches_per_step": dom["launches_per_step"],
+                "alg_flops_per_launch": dom["flops"], "alg_bytes_per_launch": dom["bytes"],
+                "traffic_source": tr["source"] if tr else None}
 
     cpu = None
     if not args.no_cpu:
@@ -342,7 +385,7 @@ def main():
         print(f"# cpu oracle: {cpu['sample']}", file=sys.stderr, flush=True)
 
     line = {
-        "metric": "action chunks/s (streaming decode step, pi0.5-shaped)",
+        "metric": METRIC,
         "value": main_res["chunks_per_s"], "unit": "chunks/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": main_res["ms_per_step"],
         "p50_us": main_res["p50_us"], "p90_us": main_res["p90_us"], "p99_us": main_res["p99_us"],

@@ -200,6 +200,18 @@ fv_status fv_set_noise_state(fv_handle h, uint64_t seed, uint64_t step);
  */
 fv_status fv_set_graph_mode(fv_handle h, int32_t enabled);
 
+/*
+ * fv_query -- host-side introspection of a handle; launches nothing.
+ *  FV_QUERY_ATTN_SPLITS: number of key ranges the attention splits each
+ *    query tile into at batch `batch` (1: no split, no combine kernel);
+ *  FV_QUERY_DEVICE_BYTES: device memory the handle holds (weights, prefix
+ *    arenas, scratch, workspace), in bytes; `batch` is ignored.
+ * `value` is a host pointer.  Errors: FV_ERR_INVALID_ARG (NULL handle or
+ * value, unknown `what`, batch outside 1..max_batch for the split query).
+ */
+enum { FV_QUERY_ATTN_SPLITS = 1, FV_QUERY_DEVICE_BYTES = 2 };
+fv_status fv_query(fv_handle h, int32_t what, int32_t batch, int64_t *value);
+
 /* fv_destroy -- synchronise the device and free everything the handle owns. */
 fv_status fv_destroy(fv_handle h);
 
@@ -229,14 +241,20 @@ fv_status fv_debug_forward(fv_handle h, const float *buffer, const float *t,
  * fv_debug_stage -- measurement aid: re-launches one kernel stage of the most
  * recent velocity pass (fv_velocity, fv_decode_step or fv_debug_forward with
  * the same batch) `reps` times on `stream`, reading the activations that pass
- * left in the handle's scratch memory.  Every stage rewrites scratch memory
- * only and gives the same result on every repetition.
+ * left in the handle's scratch memory.  Stages 0-5 rewrite scratch memory
+ * only and give the same result on every repetition; stages 6 and 7 add into
+ * the residual stream on every repetition (timing aid only: run a velocity
+ * pass again before reading results).
  *  stage 0: FiLM maps (cond -> every norm's [scale | shift | gate]);
  *  stage 1: packed QKV GEMM + rotary + K/V arena write of layer `layer`;
- *  stage 2: chunk-causal attention of layer `layer`;
- *  stage 3: packed gate/up GEMM + GeGLU (or GELU) of layer `layer`.
+ *  stage 2: chunk-causal attention of layer `layer` (both kernels);
+ *  stage 3: packed gate/up GEMM + GeGLU (or GELU) of layer `layer`;
+ *  stage 4: attention score/value kernel alone (per-split partials);
+ *  stage 5: attention split combine alone (no launch when nothing is split);
+ *  stage 6: output projection + gated residual + next FiLM RMSNorm;
+ *  stage 7: down projection + gated residual + next FiLM RMSNorm.
  * Errors: FV_ERR_STATE (no prefix), FV_ERR_INVALID_ARG (stage, layer or reps
- * out of range: reps 1..100000).
+ * out of range: stage 0..7, reps 1..100000).
  */
 fv_status fv_debug_stage(fv_handle h, int32_t stage, int32_t layer, int32_t reps, void *stream);
 

@@ -337,13 +337,13 @@ __global__ __launch_bounds__(256) void attn_combine(const T* __restrict__ part_o
 }
 
 template <typename T, int DH>
-void launch_dh(const AttnArgs& a, hipStream_t s) {
+void launch_dh(const AttnArgs& a, hipStream_t s, int parts) {
   // 32-key tiles keep wide heads (and fp32) within the register file
   constexpr int KT = (sizeof(T) == 2 && DH < 192) ? 64 : 32;
   const int G = a.n_q_heads / a.n_kv_heads;
   dim3 grid((a.tokens * G + kRowsPerBlock - 1) / kRowsPerBlock, a.B * a.n_kv_heads, a.n_split);
-  hipLaunchKernelGGL((attn_kernel<T, DH, KT, kRG>), grid, dim3(256), 0, s, a);
-  if (a.n_split > 1) {
+  if (parts & 1) hipLaunchKernelGGL((attn_kernel<T, DH, KT, kRG>), grid, dim3(256), 0, s, a);
+  if (a.n_split > 1 && (parts & 2)) {
     const int R = a.B * a.tokens * a.n_q_heads;
     hipLaunchKernelGGL((attn_combine<T, DH>), dim3((R + 3) / 4), dim3(256), 0, s,
                        reinterpret_cast<const T*>(a.part_o), a.part_ml,
@@ -359,18 +359,18 @@ int attention_row_tiles(int tokens, int n_q_heads, int n_kv_heads) {
 }
 
 template <typename T>
-void launch_attention(const AttnArgs& a, hipStream_t s) {
+void launch_attention(const AttnArgs& a, hipStream_t s, int parts) {
   switch (a.head_dim) {
-    case 64: launch_dh<T, 64>(a, s); break;
-    case 128: launch_dh<T, 128>(a, s); break;
-    case 192: launch_dh<T, 192>(a, s); break;
-    case 256: launch_dh<T, 256>(a, s); break;
+    case 64: launch_dh<T, 64>(a, s, parts); break;
+    case 128: launch_dh<T, 128>(a, s, parts); break;
+    case 192: launch_dh<T, 192>(a, s, parts); break;
+    case 256: launch_dh<T, 256>(a, s, parts); break;
     default: break;  // rejected at fv_create
   }
 }
 
-template void launch_attention<bf16_t>(const AttnArgs&, hipStream_t);
-template void launch_attention<float>(const AttnArgs&, hipStream_t);
+template void launch_attention<bf16_t>(const AttnArgs&, hipStream_t, int);
+template void launch_attention<float>(const AttnArgs&, hipStream_t, int);
 template int attention_row_tiles<bf16_t>(int, int, int);
 template int attention_row_tiles<float>(int, int, int);
 

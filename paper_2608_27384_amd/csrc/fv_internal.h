@@ -162,8 +162,9 @@ struct AttnArgs {
   float* part_ml;       // [n_split][B*tokens*Hq][2]
   int B, tokens, chunk_len, n_q_heads, n_kv_heads, head_dim, S, n_split;
 };
+// parts: bit 0 launches the score/value kernel, bit 1 the split combine.
 template <typename T>
-void launch_attention(const AttnArgs& a, hipStream_t s);
+void launch_attention(const AttnArgs& a, hipStream_t s, int parts = 3);
 template <typename T>
 int attention_row_tiles(int tokens, int n_q_heads, int n_kv_heads);
 
@@ -228,6 +229,7 @@ struct Handle {
 
   std::string last_error;
   std::vector<void*> allocations;
+  size_t device_bytes = 0;
 };
 
 }  // namespace fv

@@ -80,6 +80,7 @@ void* dalloc(Handle* h, size_t bytes) {
                          hipGetErrorString(e));
   }
   h->allocations.push_back(p);
+  h->device_bytes += bytes;
   return p;
 }
 
@@ -229,10 +230,25 @@ void run_stage(Handle* h, int stage, int l, hipStream_t s) {
       gemm_qkv<T>((T*)h->u, (const T*)h->wqkv[l], qa, rowsT, h->Nqkv, W, h->gw, s);
       break;
     }
-    case 2: {
+    case 2:
+    case 4:
+    case 5: {
       AttnArgs aa{h->q, kar, var, h->d_len, h->o, h->part_o, h->part_ml, B, h->T, h->C,
                   h->Hq, h->Hkv, h->dh, h->S, attn_split(h, B)};
-      launch_attention<T>(aa, s);
+      launch_attention<T>(aa, s, stage == 2 ? 3 : stage == 4 ? 1 : 2);
+      break;
+    }
+    case 6: {
+      const int n_attn = 2 * l, n_mlp = 2 * l + 1;
+      resid_block<T>(h, (const T*)h->o, (const T*)h->wo[l], h->Hq * h->dh, n_attn * 3 * W + 2 * W,
+                     n_mlp * 3 * W, rowsT, s);
+      break;
+    }
+    case 7: {
+      const int n_mlp = 2 * l + 1;
+      const int next_norm = l + 1 < h->L ? 2 * (l + 1) * 3 * W : -1;
+      resid_block<T>(h, (const T*)h->m, (const T*)h->wd[l], h->F, n_mlp * 3 * W + 2 * W, next_norm,
+                     rowsT, s);
       break;
     }
     default:
@@ -705,6 +721,24 @@ fv_status fv_set_graph_mode(fv_handle h, int32_t enabled) {
   });
 }
 
+fv_status fv_query(fv_handle h, int32_t what, int32_t batch, int64_t* value) {
+  if (!h) return FV_ERR_INVALID_ARG;
+  return guarded(h, [&] {
+    check_ptr(value, "value");
+    switch (what) {
+      case FV_QUERY_ATTN_SPLITS:
+        if (batch < 1 || batch > h->Bmax) fail(FV_ERR_INVALID_ARG, "batch outside 1..max_batch");
+        *value = attn_split(h, batch);
+        break;
+      case FV_QUERY_DEVICE_BYTES:
+        *value = (int64_t)h->device_bytes;
+        break;
+      default:
+        fail(FV_ERR_INVALID_ARG, "unknown query");
+    }
+  });
+}
+
 fv_status fv_debug_forward(fv_handle h, const float* buffer, const float* t, int32_t n_layers_run,
                            float* h_out, float* mod_out, void* stream) {
   if (!h) return FV_ERR_INVALID_ARG;
@@ -729,7 +763,7 @@ fv_status fv_debug_stage(fv_handle h, int32_t stage, int32_t layer, int32_t reps
   if (!h) return FV_ERR_INVALID_ARG;
   return guarded(h, [&] {
     need_prefix(h);
-    if (stage < 0 || stage > 3) fail(FV_ERR_INVALID_ARG, "stage must be 0..3");
+    if (stage < 0 || stage > 7) fail(FV_ERR_INVALID_ARG, "stage must be 0..7");
     if (layer < 0 || layer >= h->L) fail(FV_ERR_INVALID_ARG, "layer out of range");
     if (reps < 1 || reps > 100000) fail(FV_ERR_INVALID_ARG, "reps must be 1..100000");
     DeviceScope ds(h->device);

@@ -10,7 +10,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from ctypes import POINTER, c_char_p, c_float, c_int32, c_uint64, c_void_p
+from ctypes import POINTER, c_char_p, c_float, c_int32, c_int64, c_uint64, c_void_p
 from typing import Dict, Optional, Sequence
 
 import numpy as np
@@ -19,12 +19,13 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libflashvla
 
 FV_OK, FV_ERR_INVALID_ARG, FV_ERR_STATE, FV_ERR_OOM, FV_ERR_HIP, FV_ERR_INTERNAL = range(6)
 FV_BF16, FV_FP32 = 0, 1
+FV_QUERY_ATTN_SPLITS, FV_QUERY_DEVICE_BYTES = 1, 2
 
 EXPORTED = (
     "fv_create", "fv_set_prefix", "fv_decode_step", "fv_velocity", "fv_euler_shift",
     "fv_sequential_decode", "fv_get_noise_state", "fv_set_noise_state", "fv_set_graph_mode",
     "fv_destroy", "fv_status_string", "fv_last_error", "fv_abi_version", "fv_debug_forward",
-    "fv_debug_stage",
+    "fv_debug_stage", "fv_query",
 )
 
 
@@ -75,6 +76,7 @@ def lib() -> ctypes.CDLL:
             "fv_abi_version": ([], c_int32),
             "fv_debug_forward": ([H, c_void_p, c_void_p, c_int32, c_void_p, c_void_p, c_void_p], S),
             "fv_debug_stage": ([H, c_int32, c_int32, c_int32, c_void_p], S),
+            "fv_query": ([H, c_int32, c_int32, POINTER(c_int64)], S),
         }
         for name, (args, res) in sig.items():
             fn = getattr(L, name)
@@ -199,6 +201,12 @@ def fv_debug_forward(h, buffer, t, n_layers_run: int, h_out, mod_out=None, strea
                                      _ptr(mod_out), _stream(stream)), "fv_debug_forward")
 
 
+def fv_query(h, what: int, batch: int = 1) -> int:
+    val = c_int64(0)
+    _check(h, lib().fv_query(h, what, batch, ctypes.byref(val)), "fv_query")
+    return int(val.value)
+
+
 def fv_debug_stage(h, stage: int, layer: int, reps: int, stream=None) -> None:
     _check(h, lib().fv_debug_stage(h, stage, layer, reps, _stream(stream)), "fv_debug_stage")
 
@@ -218,9 +226,11 @@ class Expert:
         self.shape = shape
         self.cfg = make_cfg(shape, max_batch, max_prefix, noise_seed)
         self.handle = fv_create(weights, self.cfg)
+        self.batch = max_batch
 
     def set_prefix(self, k, v, lengths, stream=None):
         fv_set_prefix(self.handle, k, v, lengths, k.shape[2], stream)
+        self.batch = len(lengths)
 
     def decode_step(self, buffer, t, out_chunk, stream=None):
         fv_decode_step(self.handle, buffer, t, out_chunk, stream)
@@ -246,6 +256,12 @@ class Expert:
 
     def debug_forward(self, buffer, t, n_layers_run, h_out, mod_out=None, stream=None):
         fv_debug_forward(self.handle, buffer, t, n_layers_run, h_out, mod_out, stream)
+
+    def attn_split(self, batch=None) -> int:
+        return fv_query(self.handle, FV_QUERY_ATTN_SPLITS, self.batch if batch is None else batch)
+
+    def device_bytes(self) -> int:
+        return fv_query(self.handle, FV_QUERY_DEVICE_BYTES)
 
     def debug_stage(self, stage, layer, reps, stream=None):
         fv_debug_stage(self.handle, stage, layer, reps, stream)

@@ -44,6 +44,8 @@ def test_null_handle_and_null_arguments_are_rejected():
     assert L.fv_velocity(None, None, None, None, None) == fvb.FV_ERR_INVALID_ARG
     assert L.fv_destroy(None) == fvb.FV_ERR_INVALID_ARG
     assert L.fv_set_noise_state(None, 0, 0) == fvb.FV_ERR_INVALID_ARG
+    assert L.fv_query(None, fvb.FV_QUERY_ATTN_SPLITS, 1, None) == fvb.FV_ERR_INVALID_ARG
+    assert L.fv_debug_stage(None, 0, 0, 1, None) == fvb.FV_ERR_INVALID_ARG
     out = ctypes.c_void_p()
     assert L.fv_create(None, None, ctypes.byref(out)) == fvb.FV_ERR_INVALID_ARG
     assert out.value is None
