@@ -7,6 +7,7 @@ mistake anywhere in the oracle (a dropped term, a wrong sign or index, a
 transposed mask, a wrong slot shift) fails at least one of them.
 """
 import math
+import os
 
 import numpy as np
 import pytest
@@ -406,6 +407,22 @@ def test_dt_is_staircase_difference():
 
 
 # ----------------------------------------------------------------------- P14
+
+
+def test_p14_philox_known_answer_vectors():
+    """Published Philox4x32-10 known answers (tests/golden/philox4x32_10_kat.txt)."""
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                        "philox4x32_10_kat.txt")
+    n = 0
+    for line in open(path):
+        if line.startswith("#") or not line.strip():
+            continue
+        words = [int(x, 16) for x in line.split()]
+        ctr, key, want = words[:4], words[4:6], words[6:]
+        got = oracle.philox4x32_10(np.array(ctr, dtype=np.uint64), np.array(key, dtype=np.uint64))
+        assert [int(x) for x in got] == want
+        n += 1
+    assert n == 3
 
 
 def test_p14_philox_uniform_and_normal_statistics():
