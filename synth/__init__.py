@@ -13,7 +13,7 @@ value is rounded to the nearest bf16 (ties to even) before it is handed out,
 so the oracle (which upcasts to fp64) and the GPU library (which stores
 bf16) see exactly the same numbers.
 
-Workloads follow the paper's shapes: a pi0.5-style action expert (Sec. 5.1
+Workloads follow the paper's shapes: a pi0.5-style action expert (Sec. 4.1
 setup; Appendix "Model architecture"), observation prefixes of 2 or 3 camera
 views of 256 tokens plus 48 text tokens (the 2- and 3-view latency study,
 Table 2), buffers of N chunks of C actions (Sec. 3.1, Eq. 2) and the

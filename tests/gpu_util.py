@@ -36,12 +36,15 @@ def host(t):
 class Case:
     """A workload's inputs on host and device plus an open handle."""
 
-    def __init__(self, w, seed=0, weights=None, noise_seed=0, max_batch=None):
+    def __init__(self, w, seed=0, weights=None, noise_seed=0, max_batch=None, lens=None):
         from paper_2608_27384_amd.flashvla import Expert
         torch = torch_mod()
         self.w = w
         self.W = weights if weights is not None else synth.make_weights(w, seed)
         self.k, self.v, self.lens = synth.make_prefix(w, seed)
+        if lens is not None:  # explicit prefix lengths (rows past them are never visible)
+            self.lens = np.asarray(lens, dtype=np.int32)
+            assert self.lens.shape == (w.batch,) and self.lens.max() <= w.max_prefix
         self.x = synth.make_buffer(w, seed)
         self.t = synth.noise_levels_batched(w)
         self.noise_seed = noise_seed

@@ -62,6 +62,24 @@ def test_velocity_parity_small(name):
         case.close()
 
 
+@pytest.mark.parametrize("name,lens", [("small_bf16_b3", [0, 1, 90]),
+                                       ("small_fp32_b2", [0, 40])])
+def test_velocity_parity_edge_prefix_lengths(name, lens):
+    """An empty prefix (a query then sees only its own and earlier chunks), a
+    one-token prefix and the maximum prefix, in one ragged batch."""
+    w = synth.workload(name)
+    case = Case(w, lens=lens)
+    try:
+        v = case.gpu_velocity()
+        for b in range(w.batch):
+            ref = case.oracle_velocity(b)
+            errs = [rel_err(v[b, k], ref[k]) for k in range(w.n_chunks)]
+            print(name, "P =", lens[b], "max rel err", max(errs))
+            assert max(errs) < tol(w), (b, errs)
+    finally:
+        case.close()
+
+
 def test_decode_steps_lockstep_tiny():
     """Eight decode steps of the tiny fp32 config; each step the oracle takes
     the GPU's pre-step buffer, so errors do not compound."""
