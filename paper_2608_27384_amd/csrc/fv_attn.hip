@@ -31,8 +31,15 @@ namespace fv {
 namespace {
 
 constexpr float kSlack = 8.0f;  // lazy softmax reference slack (log2 units)
+constexpr float kHeadroom = 64.0f;  // fixed-reference headroom of the bf16 kernel (log2 units)
 constexpr int kRG = 1;          // 16-row MFMA groups per wave
 constexpr int kRowsPerBlock = 4 * 16 * kRG;
+constexpr int kAttn32Waves = 4;  // bf16 kernel: 4 waves x 32 rows
+
+template <typename T>
+constexpr int rows_per_block() {
+  return sizeof(T) == 2 ? 32 * kAttn32Waves : kRowsPerBlock;
+}
 
 template <typename T, int DH, int KT, int RG>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
@@ -283,6 +290,241 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
 }
 
+// bf16 path with 32x32x16 MFMAs.  A wave owns 32 query rows; S^T = K Q^T
+// gives a lane the scores of query (lane % 32) for 16 keys of a 32-key tile,
+// and those scores, rounded to bf16, are directly the B operand of
+// O^T += V^T P^T once the V^T fragment reads the same key order (lane group
+// g = lane / 32 holds keys {4g..4g+3, 8+4g..8+4g+3} of each 16-key half).
+// Per 16 k of the reduction a 32x32x16 MFMA reads 1 KB of operands for
+// 32K flops, half the LDS traffic per flop of the 16x16x32 form.
+template <int DH, int NWV>
+__global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
+  using T = bf16_t;
+  constexpr int KT = 32;                 // keys per tile
+  constexpr int NT = 64 * NWV;           // threads
+  constexpr int RB = 32 * NWV;           // query rows per block
+  constexpr int LDK = DH + 8, LDV = KT + 8;
+  constexpr int NKS = DH / 16;           // 16-wide k steps of Q K^T
+  constexpr int NDT = DH / 32;           // 32-row tiles of O^T
+  constexpr int VK = KT * DH / 8, VV = DH * KT / 8;  // 16-byte vectors per tile
+  constexpr int NVK = (VK + NT - 1) / NT, NVV = (VV + NT - 1) / NT;
+  __shared__ __attribute__((aligned(16))) T sK[KT * LDK];
+  __shared__ __attribute__((aligned(16))) T sV[DH * LDV];
+  __shared__ __attribute__((aligned(16))) T sO[NWV][32 * LDK];  // output staging
+
+  const int G = a.n_q_heads / a.n_kv_heads;
+  const int rows_bg = a.tokens * G;
+  const int tile0 = blockIdx.x * RB;
+  const int b = blockIdx.y / a.n_kv_heads, g = blockIdx.y - b * a.n_kv_heads;
+  const int split = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int P = a.len[b];
+  const int C = a.chunk_len;
+  const int l32 = lane & 31, lg = lane >> 5;
+
+  const int rq = tile0 + 32 * wave + l32;
+  const bool valid = rq < rows_bg;
+  const int rqc = valid ? rq : rows_bg - 1;
+  const int tok = rqc / G;
+  const int head = g * G + (rqc - tok * G);
+  const int lim = P + C * (tok / C + 1);
+  const int rlast = min(tile0 + RB - 1, rows_bg - 1);
+  const int lim_max = P + C * ((rlast / G) / C + 1);
+  const int nkt = (lim_max + KT - 1) / KT;
+  const int kt_begin = (split * nkt) / a.n_split, kt_end = ((split + 1) * nkt) / a.n_split;
+
+  // Q^T fragments (B operand): query l32, dh 16 ks + 8 lg .. + 8
+  bf16x8 qf[NKS];
+  {
+    const T* qrow = reinterpret_cast<const T*>(a.q) +
+                    ((size_t)(b * a.tokens + tok) * a.n_q_heads + head) * DH;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+      qf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(qrow + 16 * ks + 8 * lg));
+  }
+  f32x16 acc[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) acc[dt] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const T* kbase = reinterpret_cast<const T*>(a.karena) +
+                   ((size_t)b * a.n_kv_heads + g) * (size_t)a.S * DH;
+  const T* vbase = reinterpret_cast<const T*>(a.vtarena) +
+                   ((size_t)b * a.n_kv_heads + g) * (size_t)DH * a.S;
+  const float sl2 = 1.4426950408889634f / sqrtf((float)DH);
+
+  u32x4 rk[NVK], rv[NVV];
+  auto load_tile = [&](int kt) __attribute__((always_inline)) {
+    const int key0 = kt * KT;
+#pragma unroll
+    for (int i = 0; i < NVK; ++i) {
+      const int vi = tid + NT * i;
+      if (VK % NT == 0 || vi < VK) {
+        const int r = vi / (DH / 8), c = vi - r * (DH / 8);
+        rk[i] = *reinterpret_cast<const u32x4*>(kbase + (size_t)(key0 + r) * DH + c * 8);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NVV; ++i) {
+      const int vi = tid + NT * i;
+      if (VV % NT == 0 || vi < VV) {
+        const int r = vi / (KT / 8), c = vi - r * (KT / 8);
+        rv[i] = *reinterpret_cast<const u32x4*>(vbase + (size_t)r * a.S + key0 + c * 8);
+      }
+    }
+  };
+  auto store_tile = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < NVK; ++i) {
+      const int vi = tid + NT * i;
+      if (VK % NT == 0 || vi < VK) {
+        const int r = vi / (DH / 8), c = vi - r * (DH / 8);
+        *reinterpret_cast<u32x4*>(&sK[r * LDK + c * 8]) = rk[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NVV; ++i) {
+      const int vi = tid + NT * i;
+      if (VV % NT == 0 || vi < VV) {
+        const int r = vi / (KT / 8), c = vi - r * (KT / 8);
+        *reinterpret_cast<u32x4*>(&sV[r * LDV + c * 8]) = rv[i];
+      }
+    }
+  };
+
+  // Softmax with a fixed per-row reference m_ref: probabilities are
+  // exp2(s - m_ref) and may exceed 1 by up to 2^kHeadroom, which fp32 sums
+  // and bf16 probabilities represent exactly as well as values below 1.  The
+  // inner loop touches the accumulators only through MFMAs; when a row's
+  // score would pass the headroom (always on the first tile, rarely later)
+  // the loop stops, the accumulators are rescaled once and the same tile is
+  // processed again against the raised reference.
+  const int kt_clamp = max(kt_begin, kt_end - 1);
+  load_tile(min(kt_begin, kt_clamp));
+  int kt = kt_begin;
+  bool staged = false;  // tile kt already in LDS (after a restart)
+  float m_pending = -INFINITY;
+  while (kt < kt_end) {
+    for (; kt < kt_end; ++kt) {
+      const int key0 = kt * KT;
+      if (!staged) {
+        __syncthreads();  // previous tile fully consumed
+        store_tile();
+        __syncthreads();
+        load_tile(min(kt + 1, kt_clamp));  // overlaps the MFMA work below
+      }
+      staged = false;
+
+      // S^T (32 keys x 32 queries); lane: query l32, key 8(r/4) + 4 lg + r%4;
+      // two independent MFMA chains (even / odd k steps) halve the chain latency
+      f32x16 s0 = f32x16{}, s1 = f32x16{};
+#pragma unroll
+      for (int ks = 0; ks < NKS; ks += 2) {
+        const bf16x8 kf0 = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u16x8*>(&sK[l32 * LDK + 16 * ks + 8 * lg]));
+        const bf16x8 kf1 = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u16x8*>(&sK[l32 * LDK + 16 * ks + 16 + 8 * lg]));
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf0, qf[ks], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf1, qf[ks + 1], s1, 0, 0, 0);
+      }
+      f32x16 s = s0 + s1;
+      float mt = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = key0 + 8 * (r >> 2) + 4 * lg + (r & 3);
+        const float x = key < lim ? s[r] * sl2 : -INFINITY;
+        s[r] = x;
+        mt = fmaxf(mt, x);
+      }
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      if (__any(mt > m_run + kHeadroom)) {
+        m_pending = mt;
+        staged = true;
+        break;
+      }
+      const float m_use = m_run == -INFINITY ? 0.f : m_run;
+      float ls = 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = exp2f(s[r] - m_use);
+        s[r] = p;
+        ls += p;
+      }
+      l_run += ls + __shfl_xor(ls, 32);
+      // O^T (dh x queries) += V^T P^T over two 16-key halves
+#pragma unroll
+      for (int kc = 0; kc < 2; ++kc) {
+        u16x8 pb;
+#pragma unroll
+        for (int r = 0; r < 8; ++r) pb[r] = f32_to_bf16(s[8 * kc + r]);
+        const bf16x8 pf = __builtin_bit_cast(bf16x8, pb);
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          const T* vr = &sV[(32 * dt + l32) * LDV + 16 * kc + 4 * lg];
+          const u16x4 lo = *reinterpret_cast<const u16x4*>(vr);
+          const u16x4 hi = *reinterpret_cast<const u16x4*>(vr + 8);
+          const bf16x8 vf = __builtin_bit_cast(
+              bf16x8, u16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+          acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[dt], 0, 0, 0);
+        }
+      }
+    }
+    if (staged) {
+      // raise the reference of the rows that need it (a row's new reference
+      // is its tile maximum), rescale their accumulators, then redo tile kt
+      const float m_new = m_pending > m_run + kHeadroom ? m_pending : m_run;
+      const float alpha = m_run == -INFINITY ? 0.f : exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) acc[dt] *= alpha;
+      m_run = m_new;
+    }
+  }
+
+  // Normalised output (a split with no visible key stores 0): the wave's
+  // 32 x DH tile goes to its own LDS rows [query][dh] and then to global
+  // memory as whole rows, 16 contiguous bytes per lane.
+  const size_t R = (size_t)a.B * a.tokens * a.n_q_heads;
+  {
+    const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
+    T* so = sO[wave];
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        // registers 4q..4q+3 hold dh 32 dt + 8 q + 4 lg + 0..3
+        u16x4 w;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) w[i] = f32_to_bf16(acc[dt][4 * q + i] * inv);
+        *reinterpret_cast<u16x4*>(so + l32 * LDK + 32 * dt + 8 * q + 4 * lg) = w;
+      }
+    if (a.n_split > 1 && lg == 0 && valid) {
+      const size_t grow = (size_t)(b * a.tokens + tok) * a.n_q_heads + head;
+      a.part_ml[((size_t)split * R + grow) * 2 + 0] = m_run;
+      a.part_ml[((size_t)split * R + grow) * 2 + 1] = l_run;
+    }
+  }
+  __syncthreads();
+  {
+    constexpr int CPR = DH / 8;  // 16-byte chunks per row
+    const T* so = sO[wave];
+    for (int idx = lane; idx < 32 * CPR; idx += 64) {
+      const int row = idx / CPR, c = idx - row * CPR;
+      const int rq2 = tile0 + 32 * wave + row;
+      if (rq2 < rows_bg) {
+        const int tok2 = rq2 / G;
+        const int head2 = g * G + (rq2 - tok2 * G);
+        const size_t grow2 = (size_t)(b * a.tokens + tok2) * a.n_q_heads + head2;
+        T* orow = a.n_split == 1
+                      ? reinterpret_cast<T*>(a.o) + grow2 * DH
+                      : reinterpret_cast<T*>(a.part_o) + ((size_t)split * R + grow2) * DH;
+        *reinterpret_cast<u32x4*>(orow + 8 * c) =
+            *reinterpret_cast<const u32x4*>(so + row * LDK + 8 * c);
+      }
+    }
+  }
+}
+
 // Merge of split partials in split order.  Partial z holds o_z = acc_z / l_z
 // (stored in the element type) with its reference m_z and sum l_z:
 // o = sum_z 2^(m_z - M) l_z o_z / sum_z 2^(m_z - M) l_z.  One wave per row; a
@@ -341,8 +583,14 @@ void launch_dh(const AttnArgs& a, hipStream_t s, int parts) {
   // 32-key tiles keep wide heads (and fp32) within the register file
   constexpr int KT = (sizeof(T) == 2 && DH < 192) ? 64 : 32;
   const int G = a.n_q_heads / a.n_kv_heads;
-  dim3 grid((a.tokens * G + kRowsPerBlock - 1) / kRowsPerBlock, a.B * a.n_kv_heads, a.n_split);
-  if (parts & 1) hipLaunchKernelGGL((attn_kernel<T, DH, KT, kRG>), grid, dim3(256), 0, s, a);
+  constexpr int RB = rows_per_block<T>();
+  dim3 grid((a.tokens * G + RB - 1) / RB, a.B * a.n_kv_heads, a.n_split);
+  if (parts & 1) {
+    if constexpr (sizeof(T) == 2)
+      hipLaunchKernelGGL((attn32_kernel<DH, kAttn32Waves>), grid, dim3(64 * kAttn32Waves), 0, s, a);
+    else
+      hipLaunchKernelGGL((attn_kernel<T, DH, KT, kRG>), grid, dim3(256), 0, s, a);
+  }
   if (a.n_split > 1 && (parts & 2)) {
     const int R = a.B * a.tokens * a.n_q_heads;
     hipLaunchKernelGGL((attn_combine<T, DH>), dim3((R + 3) / 4), dim3(256), 0, s,
@@ -355,7 +603,8 @@ void launch_dh(const AttnArgs& a, hipStream_t s, int parts) {
 
 template <typename T>
 int attention_row_tiles(int tokens, int n_q_heads, int n_kv_heads) {
-  return (tokens * (n_q_heads / n_kv_heads) + kRowsPerBlock - 1) / kRowsPerBlock;
+  constexpr int RB = rows_per_block<T>();
+  return (tokens * (n_q_heads / n_kv_heads) + RB - 1) / RB;
 }
 
 template <typename T>

@@ -326,15 +326,32 @@ struct EpiQkv {
             dst[dhi] = from_f32<T>(y1);
           }
         } else {
+          // V^T rows: registers 4q..4q+3 of a lane are 4 consecutive tokens,
+          // written as one 4-element run when they are valid rows of one stream
           const int cc = c0 - qd - kd;
           const int g = cc / dh, d = cc - g * dh + (lane & 31);
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int row = row0 + 32 * i + acc_row(r, lane);
-            if (row >= M) continue;
-            T* base = a.vtarena + ((size_t)rp[r].x * a.n_kv_heads + g) * dh * a.S + rp[r].y;
-            base[(size_t)d * a.S] = from_f32<T>(acc[i][j][r]);
-            base[(size_t)(d + 32) * a.S] = from_f32<T>(acc[i][j + 1][r]);
+          for (int q = 0; q < 4; ++q) {
+            const int rowq = row0 + 32 * i + acc_row(4 * q, lane);
+            const bool run = rowq + 3 < M && rp[4 * q].x == rp[4 * q + 3].x &&
+                             (rp[4 * q].y & 3) == 0;  // aligned 4-element run
+            if (run) {
+              T* base = a.vtarena + ((size_t)rp[4 * q].x * a.n_kv_heads + g) * dh * a.S + rp[4 * q].y;
+              store4<T>(base + (size_t)d * a.S, acc[i][j][4 * q], acc[i][j][4 * q + 1],
+                        acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+              store4<T>(base + (size_t)(d + 32) * a.S, acc[i][j + 1][4 * q],
+                        acc[i][j + 1][4 * q + 1], acc[i][j + 1][4 * q + 2],
+                        acc[i][j + 1][4 * q + 3]);
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const int r = 4 * q + e;
+                if (rowq + e >= M) continue;
+                T* base = a.vtarena + ((size_t)rp[r].x * a.n_kv_heads + g) * dh * a.S + rp[r].y;
+                base[(size_t)d * a.S] = from_f32<T>(acc[i][j][r]);
+                base[(size_t)(d + 32) * a.S] = from_f32<T>(acc[i][j + 1][r]);
+              }
+            }
           }
         }
       }

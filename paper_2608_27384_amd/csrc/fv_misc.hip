@@ -49,17 +49,6 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
 }
 
 template <typename T>
-__device__ __forceinline__ void store4(T* p, float a, float b, float c, float d);
-template <>
-__device__ __forceinline__ void store4<float>(float* p, float a, float b, float c, float d) {
-  *reinterpret_cast<f32x4*>(p) = f32x4{a, b, c, d};
-}
-template <>
-__device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float a, float b, float c, float d) {
-  *reinterpret_cast<u16x4*>(p) = u16x4{f32_to_bf16(a), f32_to_bf16(b), f32_to_bf16(c), f32_to_bf16(d)};
-}
-
-template <typename T>
 __global__ __launch_bounds__(256) void embed_adarms_kernel(
     const float* __restrict__ x, const float* __restrict__ w_in, const float* __restrict__ b_in,
     float* __restrict__ h, const float* __restrict__ mod, int mod_ld, int chunk_len, float eps,

@@ -151,7 +151,9 @@ void validate_cfg(const fv_cfg& c) {
 // Key splits per attention row tile: enough blocks for two per CU (about 512),
 // at most 8 splits.
 int attn_split(const Handle* h, int B) {
-  const int base = attention_row_tiles<float>(h->T, h->Hq, h->Hkv) * B * h->Hkv;
+  const int tiles = h->bf16 ? attention_row_tiles<bf16_t>(h->T, h->Hq, h->Hkv)
+                            : attention_row_tiles<float>(h->T, h->Hq, h->Hkv);
+  const int base = tiles * B * h->Hkv;
   int s = (512 + base - 1) / base;
   return s < 1 ? 1 : (s > 8 ? 8 : s);
 }
