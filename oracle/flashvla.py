@@ -154,19 +154,49 @@ def rope_tokens(x: np.ndarray, pos: np.ndarray, theta: float) -> np.ndarray:
 # ---------------------------------------------------------------------------
 
 
+MASK_MODES = ("causal", "isolated", "bidirectional")
+
+
+def visible_chunks(chunk: int, n_chunks: int, first_valid: int = 0,
+                   mode: str = "causal") -> Tuple[int, int]:
+    """Buffer chunks [lo, hi) that the queries of ``chunk`` attend to.
+
+    * "causal" (Sec. 3.1): the chunk itself and every cleaner (earlier) valid
+      chunk, never a noisier one;
+    * "isolated" (the no-causal ablation of Appendix "Ablations"): no chunk
+      attends to another chunk, only to itself;
+    * "bidirectional": every valid chunk.
+    Slots before ``first_valid`` hold cold-start padding (Algorithm 1): they are
+    never keys of a valid chunk; a padding chunk's own queries see only
+    itself (their outputs are never used).  Every query also sees all valid
+    prefix tokens (reading R3).
+    """
+    if mode not in MASK_MODES:
+        raise ValueError(mode)
+    if chunk < first_valid or mode == "isolated":
+        return chunk, chunk + 1
+    if mode == "causal":
+        return first_valid, chunk + 1
+    return first_valid, n_chunks
+
+
 def visible_keys(chunk: int, chunk_len: int, prefix_len: int) -> Tuple[int, int]:
-    """Visible key set J(chunk): all valid prefix tokens and buffer tokens of
-    chunks 0..chunk.  Returned as (prefix count, buffer-token count)."""
-    return prefix_len, (chunk + 1) * chunk_len
+    """Visible key set J(chunk) of the causal mask with a full buffer: all
+    valid prefix tokens and buffer tokens of chunks 0..chunk.  Returned as
+    (prefix count, buffer-token count)."""
+    lo, hi = visible_chunks(chunk, chunk + 1)
+    return prefix_len, (hi - lo) * chunk_len
 
 
 def chunk_causal_attention(q: np.ndarray, k_buf: np.ndarray, v_buf: np.ndarray,
                            k_pre: np.ndarray, v_pre: np.ndarray, chunk_len: int,
-                           return_probs: bool = False):
+                           return_probs: bool = False, mode: str = "causal",
+                           first_valid: int = 0):
     """Attention of one stream's action queries.
 
     q [T, Hq, dh]; k_buf, v_buf [T, Hkv, dh]; k_pre, v_pre [P, Hkv, dh] (the
-    valid prefix only).  Query head h reads kv head h // (Hq/Hkv).  Returns o
+    valid prefix only).  Query head h reads kv head h // (Hq/Hkv).  The buffer
+    keys a chunk sees follow ``visible_chunks(mode, first_valid)``.  Returns o
     [T, Hq, dh] and, if asked, the probabilities [Hq, T, P + T] with exact
     zeros on invisible keys.
     """
@@ -180,16 +210,17 @@ def chunk_causal_attention(q: np.ndarray, k_buf: np.ndarray, v_buf: np.ndarray,
     scale = 1.0 / math.sqrt(dh)
     for k in range(K):
         rows = slice(k * chunk_len, (k + 1) * chunk_len)
-        n_pre, n_buf = visible_keys(k, chunk_len, P)
+        lo, hi = visible_chunks(k, K, first_valid, mode)
+        buf = slice(lo * chunk_len, hi * chunk_len)
         for h in range(Hq):
             g = h // group
-            keys = np.concatenate([k_pre[:n_pre, g], k_buf[:n_buf, g]], axis=0)
-            vals = np.concatenate([v_pre[:n_pre, g], v_buf[:n_buf, g]], axis=0)
+            keys = np.concatenate([k_pre[:, g], k_buf[buf, g]], axis=0)
+            vals = np.concatenate([v_pre[:, g], v_buf[buf, g]], axis=0)
             p = softmax_rows((q[rows, h] @ keys.T) * scale)
             o[rows, h] = p @ vals
             if return_probs:
-                probs[h, rows, :n_pre] = p[:, :n_pre]
-                probs[h, rows, P:P + n_buf] = p[:, n_pre:]
+                probs[h, rows, :P] = p[:, :P]
+                probs[h, rows, P + lo * chunk_len:P + hi * chunk_len] = p[:, P:]
     return (o, probs) if return_probs else o
 
 
@@ -205,14 +236,17 @@ def _chunk_broadcast(per_chunk: np.ndarray, chunk_len: int) -> np.ndarray:
 
 def velocity(x: np.ndarray, t: np.ndarray, prefix_k: np.ndarray, prefix_v: np.ndarray,
              prefix_len: int, w: Dict, cfg, dtype=np.float64,
-             trace: Optional[Dict] = None) -> np.ndarray:
+             trace: Optional[Dict] = None, mask: str = "causal",
+             first_valid: int = 0) -> np.ndarray:
     """Velocity v_theta of every chunk in one stream's buffer.
 
     x [K, C, A] buffer; t [K] per-chunk noise levels; prefix_k, prefix_v
     [L, P_max, Hkv, dh] this stream's cached observation K/V (rows < prefix_len
     valid).  ``cfg`` supplies n_layers, width, n_q_heads, n_kv_heads,
-    head_dim, mlp_dim, action_dim, rms_eps, rope_theta, mlp_gated.  Returns v
-    [K, C, A] in ``dtype``.  ``trace``, if given, receives intermediate values.
+    head_dim, mlp_dim, action_dim, rms_eps, rope_theta, mlp_gated.  ``mask``
+    and ``first_valid`` select the attention mask and the first non-padding
+    slot (see ``visible_chunks``).  Returns v [K, C, A] in ``dtype``.
+    ``trace``, if given, receives intermediate values.
     """
     K, C, A = x.shape
     L, W = cfg.n_layers, cfg.width
@@ -246,7 +280,8 @@ def velocity(x: np.ndarray, t: np.ndarray, prefix_k: np.ndarray, prefix_v: np.nd
         q = rope_tokens(q, pos, cfg.rope_theta)
         kk = rope_tokens(kk, pos, cfg.rope_theta)
         o = chunk_causal_attention(q, kk, vv, f(prefix_k[l, :prefix_len]),
-                                   f(prefix_v[l, :prefix_len]), C)
+                                   f(prefix_v[l, :prefix_len]), C, mode=mask,
+                                   first_valid=first_valid)
         h = h + g1 * (o.reshape(T, Hq * dh) @ f(w["wo"][l]))
 
         s2, b2, g2 = mods[2 * l + 1]
@@ -377,26 +412,52 @@ def gaussian_chunk(seed: int, step: int, chunk_len: int, action_dim: int) -> np.
 
 def decode_step(buffer: np.ndarray, t: np.ndarray, prefix_k: np.ndarray, prefix_v: np.ndarray,
                 prefix_len: Sequence[int], w: Dict, cfg, noise_seed: int, step: int,
-                dtype=np.float64, v_out: Optional[List] = None):
-    """One steady-streaming step for a batch of independent streams.
+                dtype=np.float64, v_out: Optional[List] = None, n_valid=None,
+                mask: str = "causal"):
+    """One streaming step for a batch of independent streams (Algorithm 1).
 
     buffer [B, K, C, A] fp32; t [B, K] (or [K]) fp32; prefix_k/v
     [L, B, P_max, Hkv, dh]; prefix_len [B].  Stream b draws its tail from
-    seed noise_seed + b at counter ``step``.  Returns (new buffer, out
-    [B, C, A]), both fp32.
+    seed noise_seed + b at counter ``step``.  ``n_valid`` [B] counts the
+    non-padding slots of each stream (the last n_valid slots; default K, the
+    steady state).  A stream whose buffer is full emits its cleanest chunk;
+    during cold start (n_valid < K) the slot popped is padding, nothing is
+    emitted (zeros: the caller executes its safe default action) and the
+    stream gains one valid slot.  Returns (new buffer, out [B, C, A]) fp32,
+    plus the new n_valid when ``n_valid`` was given.
     """
     B, K, C, A = buffer.shape
     t = np.broadcast_to(np.asarray(t, np.float32), (B, K))
+    nv = np.full(B, K, np.int64) if n_valid is None else np.asarray(n_valid, np.int64)
     new = np.empty_like(buffer)
     out = np.empty((B, C, A), np.float32)
     for b in range(B):
+        first = K - int(nv[b])
         v = velocity(buffer[b], t[b], prefix_k[:, b], prefix_v[:, b], int(prefix_len[b]),
-                     w, cfg, dtype)
+                     w, cfg, dtype, mask=mask, first_valid=first)
         if v_out is not None:
             v_out.append(v)
         tail = gaussian_chunk(noise_seed + b, step, C, A)
         new[b], out[b] = euler_emit_shift(buffer[b], t[b], v, tail)
-    return new, out
+        if first > 0:
+            out[b] = 0.0
+    if n_valid is None:
+        return new, out
+    return new, out, np.minimum(nv + 1, K)
+
+
+def cold_start(buffer: np.ndarray, streams: Sequence[int], noise_seed: int,
+               step: int) -> np.ndarray:
+    """Cold start of Algorithm 1 for the given streams: slots 0..K-2 become
+    padding (zeros) and slot K-1 a fresh N(0, I) chunk drawn at counter
+    ``step``; those streams then have one valid slot.  Returns the new
+    buffer (other streams unchanged)."""
+    new = np.array(buffer, dtype=np.float32, copy=True)
+    K, C, A = new.shape[1:]
+    for b in streams:
+        new[b, :K - 1] = 0.0
+        new[b, K - 1] = gaussian_chunk(noise_seed + b, step, C, A)
+    return new
 
 
 def sequential_levels(n_steps: int) -> np.ndarray:
