@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define FV_ABI_VERSION 1
+#define FV_ABI_VERSION 2
 
 typedef struct fv_handle_s *fv_handle;
 
@@ -51,6 +51,18 @@ typedef enum {
 } fv_status;
 
 enum { FV_BF16 = 0, FV_FP32 = 1 };
+
+/*
+ * Attention masks over the buffer (every action query also sees every valid
+ * prefix token; slots holding cold-start padding are never keys of a valid
+ * chunk, and a padding chunk's own queries see only itself):
+ *  FV_MASK_CHUNK_CAUSAL   chunk k sees chunks <= k (Sec. 3.1; the default);
+ *  FV_MASK_ISOLATED       chunk k sees only itself -- the no-causal ablation
+ *                         of Appendix "Ablations", where chunks of the buffer
+ *                         do not attend to each other;
+ *  FV_MASK_BIDIRECTIONAL  chunk k sees every valid chunk.
+ */
+enum { FV_MASK_CHUNK_CAUSAL = 0, FV_MASK_ISOLATED = 1, FV_MASK_BIDIRECTIONAL = 2 };
 
 /*
  * Shape and numerics of the action expert (Appendix "Model architecture":
@@ -133,9 +145,10 @@ fv_status fv_set_prefix(fv_handle h, const void *k, const void *v, const int32_t
                         int32_t batch, int32_t ld, void *stream);
 
 /*
- * fv_decode_step -- one steady-streaming step (Algorithm 1, steady state).
+ * fv_decode_step -- one streaming step (Algorithm 1).
  *  buffer       dev fp32 [batch][K][C][A], in/out.  Slot 0 is the cleanest chunk.
- *  t_per_chunk  dev fp32 [batch][K]: noise level of each slot (0 < t_0 < ... ).
+ *  t_per_chunk  dev fp32 [batch][K]: noise level of each slot (0 < t_0 < ... ),
+ *               or NULL to use the schedule installed by fv_set_schedule.
  *  out_chunk    dev fp32 [batch][C][A]: the emitted (executable) chunk.
  * Computes v = v_theta(buffer, t | prefix) for every chunk, then per slot
  * x'_k = x_k - dt_k v_k with dt_k = t_k - t_{k-1} (t_{-1} = 0) in fp32 (product
@@ -146,18 +159,23 @@ fv_status fv_set_prefix(fv_handle h, const void *k, const void *v, const int32_t
  * row-major [C][A] chunk, u = (r + 0.5) 2^-32, Box-Muller in fp64, rounded to
  * fp32.  Then the step counter advances by one.  With t_{K-1} = 1 and
  * t_k - dt_k = t_{k-1}, the shifted buffer sits again at t_per_chunk.
+ * A stream in cold start (fewer than K valid slots, see fv_cold_start) pops
+ * a padding slot: its out_chunk is all zeros (the caller executes its safe
+ * default action) and it gains one valid slot.
  * buffer and out_chunk must not overlap.  The first call with a new set of
  * pointers captures a HIP graph (host-synchronous); later calls replay it.
- * Errors: FV_ERR_STATE (no prefix set), FV_ERR_INVALID_ARG (NULL or
- * misaligned pointer: 16-byte alignment required), FV_ERR_HIP.
+ * Errors: FV_ERR_STATE (no prefix set; t_per_chunk NULL without a schedule
+ * for the active batch), FV_ERR_INVALID_ARG (NULL or misaligned pointer:
+ * 16-byte alignment required), FV_ERR_HIP.
  */
 fv_status fv_decode_step(fv_handle h, float *buffer, const float *t_per_chunk, float *out_chunk,
                          void *stream);
 
 /*
  * fv_velocity -- the velocity pass alone (the v_theta of Eq. 1).
- *  buffer dev fp32 [batch][K][C][A] (read only), t dev fp32 [batch][K],
- *  v_out  dev fp32 [batch][K][C][A].
+ *  buffer dev fp32 [batch][K][C][A] (read only), t dev fp32 [batch][K] (or
+ *  NULL: the installed schedule), v_out dev fp32 [batch][K][C][A].  Uses the
+ *  current mask mode and each stream's padding slots like fv_decode_step.
  * Same kernels, same order and same results as the pass inside fv_decode_step.
  * Errors: as fv_decode_step.
  */
@@ -192,6 +210,50 @@ fv_status fv_sequential_decode(fv_handle h, const float *noise, int32_t n_steps,
  */
 fv_status fv_get_noise_state(fv_handle h, uint64_t *seed, uint64_t *step);
 fv_status fv_set_noise_state(fv_handle h, uint64_t seed, uint64_t step);
+
+/*
+ * fv_set_mask_mode -- attention mask of the following passes (FV_MASK_*).
+ * Drops the captured graphs (they are captured again on next use).
+ * Errors: FV_ERR_INVALID_ARG (unknown mode).
+ */
+fv_status fv_set_mask_mode(fv_handle h, int32_t mode);
+
+/*
+ * fv_set_schedule -- static-schedule cache.  In steady state every step uses
+ * the same per-slot noise levels, so the FiLM modulation of every norm (a
+ * function of t only) is the same at every step.  Computes it once for
+ *  t dev fp32 [batch][K] (the active batch, as fv_decode_step's t_per_chunk)
+ * and keeps it, with a copy of t, in the handle; fv_decode_step and
+ * fv_velocity called with t == NULL then skip the time embedding, the
+ * time-MLP and the FiLM map products.  Results are bit-identical to passing
+ * t.  The first call allocates the cache (max_batch * K * (6L+2) * W fp32);
+ * later calls reuse it.  Stream-ordered.
+ * Errors: FV_ERR_STATE (no prefix set), FV_ERR_INVALID_ARG, FV_ERR_OOM, FV_ERR_HIP.
+ */
+fv_status fv_set_schedule(fv_handle h, const float *t, void *stream);
+
+/*
+ * fv_cold_start -- start an episode for streams [first_stream, first_stream
+ * + n_streams) of the active batch (Sec. 3.2, Algorithm 1, cold start): slots
+ * 0..K-2 of their buffer become padding chunks (zeros, never attended to by a
+ * valid chunk) and slot K-1 a fresh N(0, I) chunk drawn as fv_decode_step
+ * draws its tail, at the current step counter; the step counter then advances
+ * by one.  Those streams then have one valid slot; each fv_decode_step adds
+ * one, and the first K-1 steps emit zeros.  Other streams are untouched.
+ *  buffer dev fp32 [batch][K][C][A], in/out.  Stream-ordered; no graph.
+ * Errors: FV_ERR_STATE (no prefix set), FV_ERR_INVALID_ARG (range outside the
+ * active batch, NULL or misaligned buffer), FV_ERR_HIP.
+ */
+fv_status fv_cold_start(fv_handle h, float *buffer, int32_t first_stream, int32_t n_streams,
+                        void *stream);
+
+/*
+ * fv_get_valid_slots -- number of valid (non-padding) slots of the first
+ * `count` streams (K for a stream in steady state), into host int32
+ * out[count].  Synchronises the device.
+ * Errors: FV_ERR_INVALID_ARG (NULL out, count outside 1..max_batch).
+ */
+fv_status fv_get_valid_slots(fv_handle h, int32_t *out, int32_t count);
 
 /*
  * fv_set_graph_mode -- 1 (default): each step is one hipGraphLaunch of a

@@ -2,11 +2,13 @@
 //
 // The mask of the paper (Sec. 3.1: a noisier, later chunk attends to the
 // cleaner, earlier chunks, never the reverse, at chunk granularity; every
-// action token sees the cached observation) becomes a plain length limit
-// here: the QKV epilogue writes buffer token j of stream b at arena row
-// P_b + j, right after the P_b valid prefix rows, so a query of chunk k sees
-// exactly the key rows [0, P_b + C (k + 1)).  Rows beyond a query's limit are
-// scored -inf, giving probability exactly 0.
+// action token sees the cached observation) becomes two key ranges here:
+// the QKV epilogue writes buffer token j of stream b at arena row P_b + j,
+// right after the P_b valid prefix rows, so a query of chunk k sees the rows
+// [0, P_b) and [P_b + C lo, P_b + C hi) with (lo, hi) = (first valid slot,
+// k + 1).  The other mask modes and cold-start padding only change (lo, hi)
+// (visible_chunks).  Keys outside a query's ranges are scored -inf, giving
+// probability exactly 0; tiles outside every row's ranges are not visited.
 //
 // Work split: the query rows of one (stream, kv head) are the (token, head)
 // pairs of its query-head group, flattened token-major; a block of 4 waves
@@ -41,6 +43,27 @@ constexpr int rows_per_block() {
   return sizeof(T) == 2 ? 32 * kAttn32Waves : kRowsPerBlock;
 }
 
+// Key tiles a block visits: the prefix tiles [0, nA), then the tiles of the
+// buffer span [P + C lo_min, P + C hi_max) (the rows' visible chunk ranges
+// are monotone in the chunk index, so the first and last row of the block
+// bound them), without the masked gap between the two.
+struct KeyTiles {
+  int nA, tB0, n;
+  __device__ int tile(int vt) const { return vt < nA ? vt : tB0 + (vt - nA); }
+};
+__device__ __forceinline__ KeyTiles key_tiles(int P, int C, int K, int first, int mode,
+                                              int tok_first, int tok_last, int KT) {
+  int lo0, hi0, lo1, hi1;
+  visible_chunks(tok_first / C, K, first, mode, lo0, hi0);
+  visible_chunks(tok_last / C, K, first, mode, lo1, hi1);
+  KeyTiles r;
+  r.nA = (P + KT - 1) / KT;
+  r.tB0 = max((P + C * lo0) / KT, r.nA);
+  const int tB1 = (P + C * hi1 + KT - 1) / KT;
+  r.n = r.nA + max(0, tB1 - r.tB0);
+  return r;
+}
+
 template <typename T, int DH, int KT, int RG>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   constexpr int kRowsPerWave = 16 * RG;
@@ -70,8 +93,10 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int C = a.chunk_len;
   const int l16 = lane & 15, lg = lane >> 4;
 
-  // this lane's two query rows (one per 16-row group)
-  int tok[RG], head[RG], lim[RG];
+  const int K = a.tokens / C;
+  const int first = K - a.n_valid[b];
+  // this lane's query rows (one per 16-row group) and their buffer key ranges
+  int tok[RG], head[RG], klo[RG], khi[RG];
   bool valid[RG];
 #pragma unroll
   for (int q = 0; q < RG; ++q) {
@@ -80,12 +105,14 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     const int rqc = valid[q] ? rq : rows_bg - 1;
     tok[q] = rqc / G;
     head[q] = g * G + (rqc - tok[q] * G);
-    lim[q] = P + C * (tok[q] / C + 1);
+    int lo, hi;
+    visible_chunks(tok[q] / C, K, first, a.mask_mode, lo, hi);
+    klo[q] = P + C * lo;
+    khi[q] = P + C * hi;
   }
   const int rlast = min(tile0 + kRowsPerBlock - 1, rows_bg - 1);
-  const int lim_max = P + C * ((rlast / G) / C + 1);
-  const int nkt = (lim_max + KT - 1) / KT;
-  const int kt_begin = (split * nkt) / a.n_split, kt_end = ((split + 1) * nkt) / a.n_split;
+  const KeyTiles kts = key_tiles(P, C, K, first, a.mask_mode, tile0 / G, rlast / G, KT);
+  const int kt_begin = (split * kts.n) / a.n_split, kt_end = ((split + 1) * kts.n) / a.n_split;
 
   typename MF::frag qf[RG][NKS];
 #pragma unroll
@@ -154,13 +181,13 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   };
 
   const int kt_clamp = max(kt_begin, kt_end - 1);
-  load_tile(min(kt_begin, kt_clamp));
-  for (int kt = kt_begin; kt < kt_end; ++kt) {
-    const int key0 = kt * KT;
+  load_tile(kts.tile(min(kt_begin, kt_clamp)));
+  for (int vt = kt_begin; vt < kt_end; ++vt) {
+    const int key0 = kts.tile(vt) * KT;
     __syncthreads();  // previous tile fully consumed
     store_tile();
     __syncthreads();
-    load_tile(min(kt + 1, kt_clamp));  // overlaps the MFMA work below
+    load_tile(kts.tile(min(vt + 1, kt_clamp)));  // overlaps the MFMA work below
 
     // S^T = K Q^T for every row group; K fragments are shared
     f32x4 s[RG][NST];
@@ -191,7 +218,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int key = key0 + 16 * st + 4 * lg + r;
-          const float x = key < lim[q] ? s[q][st][r] * sl2 : -INFINITY;
+          const bool vis = key < P || (key >= klo[q] && key < khi[q]);
+          const float x = vis ? s[q][st][r] * sl2 : -INFINITY;
           s[q][st][r] = x;
           mt = fmaxf(mt, x);
         }
@@ -322,16 +350,20 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
   const int C = a.chunk_len;
   const int l32 = lane & 31, lg = lane >> 5;
 
+  const int K = a.tokens / C;
+  const int first = K - a.n_valid[b];
   const int rq = tile0 + 32 * wave + l32;
   const bool valid = rq < rows_bg;
   const int rqc = valid ? rq : rows_bg - 1;
   const int tok = rqc / G;
   const int head = g * G + (rqc - tok * G);
-  const int lim = P + C * (tok / C + 1);
+  int klo, khi;  // this row's visible buffer keys [klo, khi); prefix keys [0, P)
+  visible_chunks(tok / C, K, first, a.mask_mode, klo, khi);
+  klo = P + C * klo;
+  khi = P + C * khi;
   const int rlast = min(tile0 + RB - 1, rows_bg - 1);
-  const int lim_max = P + C * ((rlast / G) / C + 1);
-  const int nkt = (lim_max + KT - 1) / KT;
-  const int kt_begin = (split * nkt) / a.n_split, kt_end = ((split + 1) * nkt) / a.n_split;
+  const KeyTiles kts = key_tiles(P, C, K, first, a.mask_mode, tile0 / G, rlast / G, KT);
+  const int kt_begin = (split * kts.n) / a.n_split, kt_end = ((split + 1) * kts.n) / a.n_split;
 
   // Q^T fragments (B operand): query l32, dh 16 ks + 8 lg .. + 8
   bf16x8 qf[NKS];
@@ -400,18 +432,18 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
   // the loop stops, the accumulators are rescaled once and the same tile is
   // processed again against the raised reference.
   const int kt_clamp = max(kt_begin, kt_end - 1);
-  load_tile(min(kt_begin, kt_clamp));
-  int kt = kt_begin;
+  load_tile(kts.tile(min(kt_begin, kt_clamp)));
+  int kt = kt_begin;    // virtual tile index
   bool staged = false;  // tile kt already in LDS (after a restart)
   float m_pending = -INFINITY;
   while (kt < kt_end) {
     for (; kt < kt_end; ++kt) {
-      const int key0 = kt * KT;
+      const int key0 = kts.tile(kt) * KT;
       if (!staged) {
         __syncthreads();  // previous tile fully consumed
         store_tile();
         __syncthreads();
-        load_tile(min(kt + 1, kt_clamp));  // overlaps the MFMA work below
+        load_tile(kts.tile(min(kt + 1, kt_clamp)));  // overlaps the MFMA work below
       }
       staged = false;
 
@@ -432,7 +464,8 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = key0 + 8 * (r >> 2) + 4 * lg + (r & 3);
-        const float x = key < lim ? s[r] * sl2 : -INFINITY;
+        const bool vis = key < P || (key >= klo && key < khi);
+        const float x = vis ? s[r] * sl2 : -INFINITY;
         s[r] = x;
         mt = fmaxf(mt, x);
       }

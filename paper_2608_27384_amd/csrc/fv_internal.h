@@ -155,9 +155,11 @@ void launch_final(const float* h, const float* mod, int mod_ld, int scale_off, i
                   float eps, const float* w_out, const float* b_out, float* v, int rows, int W,
                   int A, hipStream_t s);
 void launch_euler_shift(float* buffer, const float* t, const float* v, float* out,
-                        const uint64_t* noise_state, uint32_t* ticket, int B, int K, int CA,
-                        hipStream_t s);
+                        const uint64_t* noise_state, uint32_t* ticket, int* n_valid, int B, int K,
+                        int CA, hipStream_t s);
 void launch_seq_euler(float* x, const float* v, const float* tsched, int j, int n, hipStream_t s);
+void launch_cold_start(float* buffer, uint64_t* noise_state, int* n_valid, int b0, int nb, int K,
+                       int CA, hipStream_t s);
 void launch_copy_f32(float* dst, const float* src, size_t n, hipStream_t s);
 void launch_fill_t(float* t, const float* tsched, int j, int B, hipStream_t s);
 template <typename T>
@@ -173,7 +175,25 @@ struct AttnArgs {
   void* part_o;         // [n_split][B*tokens*Hq][dh] element type, normalised
   float* part_ml;       // [n_split][B*tokens*Hq][2]
   int B, tokens, chunk_len, n_q_heads, n_kv_heads, head_dim, S, n_split;
+  const int* n_valid;   // [B] non-padding slots per stream (the last n_valid slots)
+  int mask_mode;        // FV_MASK_*
 };
+
+// Buffer chunks [lo, hi) visible to the queries of chunk kq (see the mask
+// modes in the C header); slots before `first` are cold-start padding.
+__host__ __device__ __forceinline__ void visible_chunks(int kq, int K, int first, int mode,
+                                                        int& lo, int& hi) {
+  if (kq < first || mode == FV_MASK_ISOLATED) {
+    lo = kq;
+    hi = kq + 1;
+  } else if (mode == FV_MASK_CHUNK_CAUSAL) {
+    lo = first;
+    hi = kq + 1;
+  } else {
+    lo = first;
+    hi = K;
+  }
+}
 // parts: bit 0 launches the score/value kernel, bit 1 the split combine.
 template <typename T>
 void launch_attention(const AttnArgs& a, hipStream_t s, int parts = 3);
@@ -231,6 +251,11 @@ struct Handle {
 
   GemmWork gw;                    // split-K workspace and counters
   uint64_t* d_noise = nullptr;   // {seed, step}
+  int* d_valid = nullptr;        // [Bmax] non-padding slots per stream (K: steady state)
+  int mask_mode = FV_MASK_CHUNK_CAUSAL;
+  float* mod_cache = nullptr;    // [Bmax*K][Nmod] FiLM maps of a static schedule
+  float* t_cache = nullptr;      // [Bmax*K] the schedule itself
+  int sched_batch = 0;           // batch the cached schedule was made for (0: none)
   uint32_t* d_ticket = nullptr;
 
   // graphs

@@ -325,7 +325,8 @@ __global__ __launch_bounds__(256) void euler_shift_kernel(float* __restrict__ bu
                                                           const float* __restrict__ v,
                                                           float* __restrict__ out,
                                                           uint64_t* __restrict__ noise_state,
-                                                          uint32_t* __restrict__ ticket, int B,
+                                                          uint32_t* __restrict__ ticket,
+                                                          int* __restrict__ n_valid, int B,
                                                           int K, int CA) {
   // The update must round the product and the difference separately.
 #pragma clang fp contract(off)
@@ -337,11 +338,13 @@ __global__ __launch_bounds__(256) void euler_shift_kernel(float* __restrict__ bu
   const bool active = jl < gpb && gid < B * groups;
   float xn[4] = {0.f, 0.f, 0.f, 0.f};
   int b = 0, j = 0, e0 = 0, ne = 0;
+  bool full = true;  // the popped slot holds a real chunk (not cold-start padding)
   if (active) {
     b = gid / groups;
     j = gid - b * groups;
     e0 = 4 * j;
     ne = min(4, CA - e0);
+    full = n_valid[b] >= K;
     const float tk = t[(size_t)b * K + k];
     const float tp = k > 0 ? t[(size_t)b * K + k - 1] : 0.f;
     const float dt = tk - tp;
@@ -355,7 +358,7 @@ __global__ __launch_bounds__(256) void euler_shift_kernel(float* __restrict__ bu
   if (active) {
     const size_t base = ((size_t)b * K + k) * CA + e0;
     if (k == 0) {
-      for (int i = 0; i < ne; ++i) out[(size_t)b * CA + e0 + i] = xn[i];
+      for (int i = 0; i < ne; ++i) out[(size_t)b * CA + e0 + i] = full ? xn[i] : 0.f;
     } else {
       for (int i = 0; i < ne; ++i) buf[base - CA + i] = xn[i];
     }
@@ -369,16 +372,54 @@ __global__ __launch_bounds__(256) void euler_shift_kernel(float* __restrict__ bu
       for (int i = 0; i < ne; ++i) buf[base + i] = z[i];
     }
   }
-  // step counter: advanced once every block has read it
+  // step counter and valid-slot counts: advanced by the last block, once
+  // every block has read them
+  __shared__ int s_last;
   __syncthreads();
   if (threadIdx.x == 0) {
     const uint32_t done =
         __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    if (done == gridDim.x - 1) {
+    s_last = done == gridDim.x - 1;
+    if (s_last) {
       noise_state[1] = step + 1;
       __hip_atomic_store(ticket, 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
+  __syncthreads();
+  if (s_last)
+    for (int bb = threadIdx.x; bb < B; bb += blockDim.x) n_valid[bb] = min(n_valid[bb] + 1, K);
+}
+
+// Cold start of streams [b0, b0 + nb): slots 0..K-2 become zero padding, slot
+// K-1 a fresh Gaussian chunk drawn as euler_shift_kernel draws its tail (at
+// the current step); then the step counter advances and those streams hold
+// one valid slot.  One block.
+__global__ __launch_bounds__(256) void cold_start_kernel(float* __restrict__ buf,
+                                                         uint64_t* __restrict__ noise_state,
+                                                         int* __restrict__ n_valid, int b0,
+                                                         int nb, int K, int CA) {
+  const uint64_t seed = noise_state[0], step = noise_state[1];
+  const int groups = (CA + 3) >> 2;
+  for (int idx = threadIdx.x; idx < nb * K * groups; idx += blockDim.x) {
+    const int bl = idx / (K * groups), rem = idx - bl * (K * groups);
+    const int k = rem / groups, j = rem - k * groups;
+    const int b = b0 + bl, e0 = 4 * j, ne = min(4, CA - e0);
+    float* dst = buf + ((size_t)b * K + k) * CA + e0;
+    if (k < K - 1) {
+      for (int i = 0; i < ne; ++i) dst[i] = 0.f;
+    } else {
+      uint32_t c[4] = {(uint32_t)j, (uint32_t)step, (uint32_t)(step >> 32), 0u};
+      const uint64_t sb = seed + (uint64_t)b;
+      philox4x32_10(c, (uint32_t)sb, (uint32_t)(sb >> 32));
+      float z[4];
+      box_muller(c[0], c[1], &z[0], &z[1]);
+      box_muller(c[2], c[3], &z[2], &z[3]);
+      for (int i = 0; i < ne; ++i) dst[i] = z[i];
+    }
+  }
+  __syncthreads();  // every thread has read the step counter
+  if (threadIdx.x == 0) noise_state[1] = step + 1;
+  for (int bl = threadIdx.x; bl < nb; bl += blockDim.x) n_valid[b0 + bl] = 1;
 }
 
 // x <- x - (t_j - t_{j+1}) v   (sequential decode; product then difference rounded)
@@ -486,13 +527,19 @@ void launch_final(const float* h, const float* mod, int mod_ld, int scale_off, i
 }
 
 void launch_euler_shift(float* buffer, const float* t, const float* v, float* out,
-                        const uint64_t* noise_state, uint32_t* ticket, int B, int K, int CA,
-                        hipStream_t s) {
+                        const uint64_t* noise_state, uint32_t* ticket, int* n_valid, int B, int K,
+                        int CA, hipStream_t s) {
   const int groups = (CA + 3) / 4;
   const int gpb = 256 / K;
   const int n = B * groups;
   hipLaunchKernelGGL(euler_shift_kernel, dim3((n + gpb - 1) / gpb), dim3(256), 0, s, buffer, t, v,
-                     out, const_cast<uint64_t*>(noise_state), ticket, B, K, CA);
+                     out, const_cast<uint64_t*>(noise_state), ticket, n_valid, B, K, CA);
+}
+
+void launch_cold_start(float* buffer, uint64_t* noise_state, int* n_valid, int b0, int nb, int K,
+                       int CA, hipStream_t s) {
+  hipLaunchKernelGGL(cold_start_kernel, dim3(1), dim3(256), 0, s, buffer, noise_state, n_valid, b0,
+                     nb, K, CA);
 }
 
 void launch_seq_euler(float* x, const float* v, const float* tsched, int j, int n,

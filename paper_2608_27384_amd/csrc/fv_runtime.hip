@@ -162,33 +162,52 @@ int attn_split(const Handle* h, int B) {
 // Output projection / down projection with the gated residual, fused with
 // the FiLM RMSNorm that feeds the next GEMM (norm_off < 0: none).
 template <typename T>
-void resid_block(Handle* h, const T* A, const T* Bt, int K, int gate_off, int norm_off,
-                 int rowsT, hipStream_t s) {
+void resid_block(Handle* h, const float* mod, const T* A, const T* Bt, int K, int gate_off,
+                 int norm_off, int rowsT, hipStream_t s) {
   const int W = h->W;
   const int ks = gemm_partials<T>(A, Bt, rowsT, W, K, h->gw, s);
   if (ks > 1) {
-    launch_resid_norm<T>(h->gw.ws, ks, h->hres, h->mod, h->Nmod, gate_off, norm_off, h->C,
+    launch_resid_norm<T>(h->gw.ws, ks, h->hres, mod, h->Nmod, gate_off, norm_off, h->C,
                          h->cfg.rms_eps, (T*)h->u, rowsT, W, s);
   } else {
-    gemm_gated_resid<T>(A, Bt, h->hres, h->mod, h->Nmod, gate_off, h->C, rowsT, W, K, h->gw, s);
+    gemm_gated_resid<T>(A, Bt, h->hres, mod, h->Nmod, gate_off, h->C, rowsT, W, K, h->gw, s);
     if (norm_off >= 0)
-      launch_adarms<T>(h->hres, h->mod, h->Nmod, norm_off, h->C, h->cfg.rms_eps, (T*)h->u, rowsT,
+      launch_adarms<T>(h->hres, mod, h->Nmod, norm_off, h->C, h->cfg.rms_eps, (T*)h->u, rowsT,
                        W, s);
   }
 }
 
+// FiLM maps of every norm for noise levels t [B*K]: timestep embedding,
+// time-MLP, one GEMM for all (2L+1) [scale | shift | gate] maps -> mod.
 template <typename T>
-void enqueue_forward(Handle* h, const float* buffer, const float* t, int B, float* v_out,
-                     int n_layers_run, hipStream_t s) {
-  const int W = h->W, rowsK = B * h->K, rowsT = B * h->T;
-  const int Nmod = h->Nmod;
-  const size_t layer_elems = (size_t)h->Bmax * h->Hkv * h->S * h->dh;
+void enqueue_film_maps(Handle* h, const float* t, int B, float* mod, hipStream_t s) {
+  const int W = h->W, rowsK = B * h->K;
   launch_time_embed<T>(t, (T*)h->e, rowsK, W, s);
   gemm_bias_silu<T>((T*)h->e, (T*)h->w_t1, h->b_t1, (T*)h->hid, rowsK, W, W, h->gw, s);
   gemm_bias_silu<T>((T*)h->hid, (T*)h->w_t2, h->b_t2, (T*)h->cond, rowsK, W, W, h->gw, s);
-  gemm_bias_f32<T>((T*)h->cond, (T*)h->w_mod, h->b_mod, h->mod, rowsK, Nmod, W, h->gw, s);
+  gemm_bias_f32<T>((T*)h->cond, (T*)h->w_mod, h->b_mod, mod, rowsK, h->Nmod, W, h->gw, s);
+}
+
+AttnArgs attn_args(const Handle* h, const void* kar, const void* var, int B, int n_split) {
+  return AttnArgs{h->q, kar, var, h->d_len, h->o, h->part_o, h->part_ml, B, h->T, h->C, h->Hq,
+                  h->Hkv, h->dh, h->S, n_split, h->d_valid, h->mask_mode};
+}
+
+// Velocity pass.  `mod_cached` (FiLM maps of a static schedule) replaces the
+// time conditioning of t when given.
+template <typename T>
+void enqueue_forward(Handle* h, const float* buffer, const float* t, int B, float* v_out,
+                     int n_layers_run, hipStream_t s, const float* mod_cached) {
+  const int W = h->W, rowsT = B * h->T;
+  const int Nmod = h->Nmod;
+  const size_t layer_elems = (size_t)h->Bmax * h->Hkv * h->S * h->dh;
+  const float* mod = mod_cached;
+  if (!mod) {
+    enqueue_film_maps<T>(h, t, B, h->mod, s);
+    mod = h->mod;
+  }
   launch_row_pos(h->d_len, h->row_pos, rowsT, h->T, s);
-  launch_embed_adarms<T>(buffer, h->w_in, h->b_in, h->hres, h->mod, Nmod, h->C, h->cfg.rms_eps,
+  launch_embed_adarms<T>(buffer, h->w_in, h->b_in, h->hres, mod, Nmod, h->C, h->cfg.rms_eps,
                          (T*)h->u, rowsT, h->A, W, s);
   const int n_split = attn_split(h, B);
   for (int l = 0; l < n_layers_run; ++l) {
@@ -198,21 +217,19 @@ void enqueue_forward(Handle* h, const float* buffer, const float* t, int B, floa
     QkvArgs<T> qa{(T*)h->q, kar, var, h->rcos, h->rsin, h->row_pos, h->T, h->Hq, h->Hkv, h->dh,
                   h->S};
     gemm_qkv<T>((T*)h->u, (const T*)h->wqkv[l], qa, rowsT, h->Nqkv, W, h->gw, s);
-    AttnArgs aa{h->q, kar, var, h->d_len, h->o, h->part_o, h->part_ml, B, h->T, h->C,
-                h->Hq, h->Hkv, h->dh, h->S, n_split};
-    launch_attention<T>(aa, s);
-    resid_block<T>(h, (const T*)h->o, (const T*)h->wo[l], h->Hq * h->dh, n_attn * 3 * W + 2 * W,
-                   n_mlp * 3 * W, rowsT, s);
+    launch_attention<T>(attn_args(h, kar, var, B, n_split), s);
+    resid_block<T>(h, mod, (const T*)h->o, (const T*)h->wo[l], h->Hq * h->dh,
+                   n_attn * 3 * W + 2 * W, n_mlp * 3 * W, rowsT, s);
     if (h->cfg.mlp_gated)
       gemm_geglu<T>((T*)h->u, (const T*)h->wgu[l], (T*)h->m, rowsT, h->Ngu, W, h->gw, s);
     else
       gemm_gelu<T>((T*)h->u, (const T*)h->wgu[l], (T*)h->m, rowsT, h->Ngu, W, h->gw, s);
     const int next_norm = l + 1 < h->L ? 2 * (l + 1) * 3 * W : -1;
-    resid_block<T>(h, (const T*)h->m, (const T*)h->wd[l], h->F, n_mlp * 3 * W + 2 * W, next_norm,
-                   rowsT, s);
+    resid_block<T>(h, mod, (const T*)h->m, (const T*)h->wd[l], h->F, n_mlp * 3 * W + 2 * W,
+                   next_norm, rowsT, s);
   }
   if (v_out)
-    launch_final(h->hres, h->mod, Nmod, 6 * h->L * W, h->C, h->cfg.rms_eps, h->w_out, h->b_out,
+    launch_final(h->hres, mod, Nmod, 6 * h->L * W, h->C, h->cfg.rms_eps, h->w_out, h->b_out,
                  v_out, rowsT, W, h->A, s);
 }
 
@@ -235,22 +252,21 @@ void run_stage(Handle* h, int stage, int l, hipStream_t s) {
     case 2:
     case 4:
     case 5: {
-      AttnArgs aa{h->q, kar, var, h->d_len, h->o, h->part_o, h->part_ml, B, h->T, h->C,
-                  h->Hq, h->Hkv, h->dh, h->S, attn_split(h, B)};
-      launch_attention<T>(aa, s, stage == 2 ? 3 : stage == 4 ? 1 : 2);
+      launch_attention<T>(attn_args(h, kar, var, B, attn_split(h, B)), s,
+                          stage == 2 ? 3 : stage == 4 ? 1 : 2);
       break;
     }
     case 6: {
       const int n_attn = 2 * l, n_mlp = 2 * l + 1;
-      resid_block<T>(h, (const T*)h->o, (const T*)h->wo[l], h->Hq * h->dh, n_attn * 3 * W + 2 * W,
-                     n_mlp * 3 * W, rowsT, s);
+      resid_block<T>(h, h->mod, (const T*)h->o, (const T*)h->wo[l], h->Hq * h->dh,
+                     n_attn * 3 * W + 2 * W, n_mlp * 3 * W, rowsT, s);
       break;
     }
     case 7: {
       const int n_mlp = 2 * l + 1;
       const int next_norm = l + 1 < h->L ? 2 * (l + 1) * 3 * W : -1;
-      resid_block<T>(h, (const T*)h->m, (const T*)h->wd[l], h->F, n_mlp * 3 * W + 2 * W, next_norm,
-                     rowsT, s);
+      resid_block<T>(h, h->mod, (const T*)h->m, (const T*)h->wd[l], h->F, n_mlp * 3 * W + 2 * W,
+                     next_norm, rowsT, s);
       break;
     }
     default:
@@ -262,11 +278,18 @@ void run_stage(Handle* h, int stage, int l, hipStream_t s) {
 }
 
 void forward(Handle* h, const float* buffer, const float* t, int B, float* v_out, int n_layers,
-             hipStream_t s) {
+             hipStream_t s, const float* mod_cached = nullptr) {
   if (h->bf16)
-    enqueue_forward<bf16_t>(h, buffer, t, B, v_out, n_layers, s);
+    enqueue_forward<bf16_t>(h, buffer, t, B, v_out, n_layers, s, mod_cached);
   else
-    enqueue_forward<float>(h, buffer, t, B, v_out, n_layers, s);
+    enqueue_forward<float>(h, buffer, t, B, v_out, n_layers, s, mod_cached);
+}
+
+void film_maps(Handle* h, const float* t, int B, float* mod, hipStream_t s) {
+  if (h->bf16)
+    enqueue_film_maps<bf16_t>(h, t, B, mod, s);
+  else
+    enqueue_film_maps<float>(h, t, B, mod, s);
 }
 
 void check_launch() {
@@ -348,7 +371,26 @@ void need_prefix(const Handle* h) {
   if (!h->prefix_set) fail(FV_ERR_STATE, "no observation prefix: call fv_set_prefix first");
 }
 
-enum Kind { KIND_STEP = 1, KIND_VELOCITY = 2, KIND_SEQ = 3 };
+enum Kind { KIND_STEP = 1, KIND_VELOCITY = 2, KIND_SEQ = 3, KIND_STEP_CACHED = 4,
+            KIND_VELOCITY_CACHED = 5 };
+
+// The noise levels a pass uses: the caller's t, or the installed schedule.
+const float* schedule_or(const Handle* h, const float* t) {
+  if (t) return t;
+  if (h->sched_batch != h->batch)
+    fail(FV_ERR_STATE, "t is NULL but no schedule is installed for the active batch "
+                       "(call fv_set_schedule)");
+  return h->t_cache;
+}
+
+// Drops the captured graphs (their kernel arguments are out of date).
+void clear_graphs(Handle* h) {
+  if (h->graphs.empty()) return;
+  (void)hipDeviceSynchronize();
+  for (GraphEntry& g : h->graphs)
+    if (g.exec) (void)hipGraphExecDestroy(g.exec);
+  h->graphs.clear();
+}
 
 void destroy_handle(Handle* h) {
   if (h->allocations.empty() && !h->cap_stream && h->graphs.empty()) return;
@@ -514,6 +556,11 @@ fv_status fv_create(const fv_weights* w, const fv_cfg* cfg, fv_handle* out) {
     FV_HIP(hipMemset(H.vtarena, 0, arena));
     H.d_len = static_cast<int*>(dalloc(h, (size_t)H.Bmax * 4));
     FV_HIP(hipMemset(H.d_len, 0, (size_t)H.Bmax * 4));
+    {
+      const std::vector<int> full(H.Bmax, H.K);  // every stream starts in steady state
+      H.d_valid = static_cast<int*>(dalloc(h, (size_t)H.Bmax * 4));
+      FV_HIP(hipMemcpy(H.d_valid, full.data(), (size_t)H.Bmax * 4, hipMemcpyHostToDevice));
+    }
     const size_t rowsK = (size_t)H.Bmax * H.K, rowsT = (size_t)H.Bmax * H.T;
     H.e = dalloc(h, rowsK * W * H.esz);
     H.hid = dalloc(h, rowsK * W * H.esz);
@@ -608,17 +655,19 @@ fv_status fv_decode_step(fv_handle h, float* buffer, const float* t, float* out_
   return guarded(h, [&] {
     need_prefix(h);
     check_ptr(buffer, "buffer");
-    check_ptr(t, "t_per_chunk");
+    if (t) check_ptr(t, "t_per_chunk");
     check_ptr(out_chunk, "out_chunk");
+    const float* tt = schedule_or(h, t);
+    const float* mod = t ? nullptr : h->mod_cache;
     const int B = h->batch;
     const size_t nbuf = (size_t)B * h->T * h->A * 4, nout = (size_t)B * h->C * h->A * 4;
     if (overlap(buffer, nbuf, out_chunk, nout)) fail(FV_ERR_INVALID_ARG, "buffer and out_chunk overlap");
     DeviceScope ds(h->device);
-    run_step(h, KIND_STEP, buffer, t, out_chunk, nullptr, 0, static_cast<hipStream_t>(stream),
-             [&](hipStream_t s) {
-               forward(h, buffer, t, B, h->v, h->L, s);
-               launch_euler_shift(buffer, t, h->v, out_chunk, h->d_noise, h->d_ticket, B, h->K,
-                                  h->C * h->A, s);
+    run_step(h, t ? KIND_STEP : KIND_STEP_CACHED, buffer, tt, out_chunk, nullptr, 0,
+             static_cast<hipStream_t>(stream), [&](hipStream_t s) {
+               forward(h, buffer, tt, B, h->v, h->L, s, mod);
+               launch_euler_shift(buffer, tt, h->v, out_chunk, h->d_noise, h->d_ticket,
+                                  h->d_valid, B, h->K, h->C * h->A, s);
              });
   });
 }
@@ -629,12 +678,15 @@ fv_status fv_velocity(fv_handle h, const float* buffer, const float* t, float* v
   return guarded(h, [&] {
     need_prefix(h);
     check_ptr(buffer, "buffer");
-    check_ptr(t, "t");
+    if (t) check_ptr(t, "t");
     check_ptr(v_out, "v_out");
+    const float* tt = schedule_or(h, t);
+    const float* mod = t ? nullptr : h->mod_cache;
     const int B = h->batch;
     DeviceScope ds(h->device);
-    run_step(h, KIND_VELOCITY, buffer, t, v_out, nullptr, 0, static_cast<hipStream_t>(stream),
-             [&](hipStream_t s) { forward(h, buffer, t, B, v_out, h->L, s); });
+    run_step(h, t ? KIND_VELOCITY : KIND_VELOCITY_CACHED, buffer, tt, v_out, nullptr, 0,
+             static_cast<hipStream_t>(stream),
+             [&](hipStream_t s) { forward(h, buffer, tt, B, v_out, h->L, s, mod); });
   });
 }
 
@@ -651,8 +703,8 @@ fv_status fv_euler_shift(fv_handle h, float* buffer, const float* t, const float
     if (overlap(buffer, nbuf, out_chunk, nout)) fail(FV_ERR_INVALID_ARG, "buffer and out_chunk overlap");
     DeviceScope ds(h->device);
     (void)hipGetLastError();
-    launch_euler_shift(buffer, t, v, out_chunk, h->d_noise, h->d_ticket, B, h->K, h->C * h->A,
-                       static_cast<hipStream_t>(stream));
+    launch_euler_shift(buffer, t, v, out_chunk, h->d_noise, h->d_ticket, h->d_valid, B, h->K,
+                       h->C * h->A, static_cast<hipStream_t>(stream));
     check_launch();
   });
 }
@@ -688,6 +740,65 @@ fv_status fv_sequential_decode(fv_handle h, const float* noise, int32_t n_steps,
                }
                launch_copy_f32(out_chunk, h->seq_x, n, s);
              });
+  });
+}
+
+fv_status fv_set_mask_mode(fv_handle h, int32_t mode) {
+  if (!h) return FV_ERR_INVALID_ARG;
+  return guarded(h, [&] {
+    if (mode != FV_MASK_CHUNK_CAUSAL && mode != FV_MASK_ISOLATED && mode != FV_MASK_BIDIRECTIONAL)
+      fail(FV_ERR_INVALID_ARG, "unknown mask mode");
+    if (mode == h->mask_mode) return;
+    DeviceScope ds(h->device);
+    clear_graphs(h);
+    h->mask_mode = mode;
+  });
+}
+
+fv_status fv_set_schedule(fv_handle h, const float* t, void* stream) {
+  if (!h) return FV_ERR_INVALID_ARG;
+  return guarded(h, [&] {
+    need_prefix(h);
+    check_ptr(t, "t");
+    DeviceScope ds(h->device);
+    if (!h->mod_cache) {
+      h->mod_cache = static_cast<float*>(dalloc(h, (size_t)h->Bmax * h->K * h->Nmod * 4));
+      h->t_cache = static_cast<float*>(dalloc(h, (size_t)h->Bmax * h->K * 4));
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    const int B = h->batch;
+    launch_copy_f32(h->t_cache, t, (size_t)B * h->K, s);
+    film_maps(h, h->t_cache, B, h->mod_cache, s);
+    check_launch();
+    h->sched_batch = B;
+  });
+}
+
+fv_status fv_cold_start(fv_handle h, float* buffer, int32_t first_stream, int32_t n_streams,
+                        void* stream) {
+  if (!h) return FV_ERR_INVALID_ARG;
+  return guarded(h, [&] {
+    need_prefix(h);
+    check_ptr(buffer, "buffer");
+    if (first_stream < 0 || n_streams < 1 || first_stream + n_streams > h->batch)
+      fail(FV_ERR_INVALID_ARG, "stream range outside the active batch");
+    DeviceScope ds(h->device);
+    (void)hipGetLastError();
+    launch_cold_start(buffer, h->d_noise, h->d_valid, first_stream, n_streams, h->K, h->C * h->A,
+                      static_cast<hipStream_t>(stream));
+    check_launch();
+  });
+}
+
+fv_status fv_get_valid_slots(fv_handle h, int32_t* out, int32_t count) {
+  if (!h) return FV_ERR_INVALID_ARG;
+  return guarded(h, [&] {
+    need(out, "out");
+    if (count < 1 || count > h->Bmax) fail(FV_ERR_INVALID_ARG, "count outside 1..max_batch");
+    DeviceScope ds(h->device);
+    FV_HIP(hipDeviceSynchronize());
+    FV_HIP(hipMemcpy(out, h->d_valid, (size_t)count * 4, hipMemcpyDeviceToHost));
   });
 }
 

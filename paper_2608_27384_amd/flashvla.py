@@ -20,12 +20,16 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libflashvla
 FV_OK, FV_ERR_INVALID_ARG, FV_ERR_STATE, FV_ERR_OOM, FV_ERR_HIP, FV_ERR_INTERNAL = range(6)
 FV_BF16, FV_FP32 = 0, 1
 FV_QUERY_ATTN_SPLITS, FV_QUERY_DEVICE_BYTES = 1, 2
+FV_MASK_CHUNK_CAUSAL, FV_MASK_ISOLATED, FV_MASK_BIDIRECTIONAL = 0, 1, 2
+MASK_MODES = {"causal": FV_MASK_CHUNK_CAUSAL, "isolated": FV_MASK_ISOLATED,
+              "bidirectional": FV_MASK_BIDIRECTIONAL}
 
 EXPORTED = (
     "fv_create", "fv_set_prefix", "fv_decode_step", "fv_velocity", "fv_euler_shift",
     "fv_sequential_decode", "fv_get_noise_state", "fv_set_noise_state", "fv_set_graph_mode",
     "fv_destroy", "fv_status_string", "fv_last_error", "fv_abi_version", "fv_debug_forward",
-    "fv_debug_stage", "fv_query",
+    "fv_debug_stage", "fv_query", "fv_set_mask_mode", "fv_set_schedule", "fv_cold_start",
+    "fv_get_valid_slots",
 )
 
 
@@ -77,6 +81,10 @@ def lib() -> ctypes.CDLL:
             "fv_debug_forward": ([H, c_void_p, c_void_p, c_int32, c_void_p, c_void_p, c_void_p], S),
             "fv_debug_stage": ([H, c_int32, c_int32, c_int32, c_void_p], S),
             "fv_query": ([H, c_int32, c_int32, POINTER(c_int64)], S),
+            "fv_set_mask_mode": ([H, c_int32], S),
+            "fv_set_schedule": ([H, c_void_p, c_void_p], S),
+            "fv_cold_start": ([H, c_void_p, c_int32, c_int32, c_void_p], S),
+            "fv_get_valid_slots": ([H, POINTER(c_int32), c_int32], S),
         }
         for name, (args, res) in sig.items():
             fn = getattr(L, name)
@@ -201,6 +209,25 @@ def fv_debug_forward(h, buffer, t, n_layers_run: int, h_out, mod_out=None, strea
                                      _ptr(mod_out), _stream(stream)), "fv_debug_forward")
 
 
+def fv_set_mask_mode(h, mode: int) -> None:
+    _check(h, lib().fv_set_mask_mode(h, mode), "fv_set_mask_mode")
+
+
+def fv_set_schedule(h, t, stream=None) -> None:
+    _check(h, lib().fv_set_schedule(h, _ptr(t), _stream(stream)), "fv_set_schedule")
+
+
+def fv_cold_start(h, buffer, first_stream: int, n_streams: int, stream=None) -> None:
+    _check(h, lib().fv_cold_start(h, _ptr(buffer), first_stream, n_streams, _stream(stream)),
+           "fv_cold_start")
+
+
+def fv_get_valid_slots(h, count: int):
+    arr = (c_int32 * count)()
+    _check(h, lib().fv_get_valid_slots(h, arr, count), "fv_get_valid_slots")
+    return [int(x) for x in arr]
+
+
 def fv_query(h, what: int, batch: int = 1) -> int:
     val = c_int64(0)
     _check(h, lib().fv_query(h, what, batch, ctypes.byref(val)), "fv_query")
@@ -256,6 +283,19 @@ class Expert:
 
     def debug_forward(self, buffer, t, n_layers_run, h_out, mod_out=None, stream=None):
         fv_debug_forward(self.handle, buffer, t, n_layers_run, h_out, mod_out, stream)
+
+    def set_mask_mode(self, mode):
+        fv_set_mask_mode(self.handle, MASK_MODES[mode] if isinstance(mode, str) else mode)
+
+    def set_schedule(self, t, stream=None):
+        fv_set_schedule(self.handle, t, stream)
+
+    def cold_start(self, buffer, first_stream=0, n_streams=None, stream=None):
+        n = self.batch - first_stream if n_streams is None else n_streams
+        fv_cold_start(self.handle, buffer, first_stream, n, stream)
+
+    def valid_slots(self, count=None):
+        return fv_get_valid_slots(self.handle, self.batch if count is None else count)
 
     def attn_split(self, batch=None) -> int:
         return fv_query(self.handle, FV_QUERY_ATTN_SPLITS, self.batch if batch is None else batch)

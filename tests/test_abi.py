@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     L = fvb.lib()
     for name in _declared():
         assert hasattr(L, name), name
-    assert L.fv_abi_version() == 1
+    assert L.fv_abi_version() == 2
 
 
 def test_status_strings():
@@ -46,6 +46,10 @@ def test_null_handle_and_null_arguments_are_rejected():
     assert L.fv_set_noise_state(None, 0, 0) == fvb.FV_ERR_INVALID_ARG
     assert L.fv_query(None, fvb.FV_QUERY_ATTN_SPLITS, 1, None) == fvb.FV_ERR_INVALID_ARG
     assert L.fv_debug_stage(None, 0, 0, 1, None) == fvb.FV_ERR_INVALID_ARG
+    assert L.fv_set_mask_mode(None, 0) == fvb.FV_ERR_INVALID_ARG
+    assert L.fv_set_schedule(None, None, None) == fvb.FV_ERR_INVALID_ARG
+    assert L.fv_cold_start(None, None, 0, 1, None) == fvb.FV_ERR_INVALID_ARG
+    assert L.fv_get_valid_slots(None, None, 1) == fvb.FV_ERR_INVALID_ARG
     out = ctypes.c_void_p()
     assert L.fv_create(None, None, ctypes.byref(out)) == fvb.FV_ERR_INVALID_ARG
     assert out.value is None
