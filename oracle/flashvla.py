@@ -460,6 +460,25 @@ def cold_start(buffer: np.ndarray, streams: Sequence[int], noise_seed: int,
     return new
 
 
+def multibuffer_velocity(buffers: np.ndarray, t: np.ndarray, prefix_k: np.ndarray,
+                         prefix_v: np.ndarray, prefix_len: int, w: Dict, cfg,
+                         dtype=np.float64, mask: str = "causal") -> np.ndarray:
+    """Forward of the packed multi-buffer sample of Sec. 3.3 for one observation.
+
+    buffers [N, N, C, A]: configuration j = 1..N is buffers[j-1], whose slots
+    0..N-j-1 hold padding and slots N-j..N-1 the j real (noised) chunks; t
+    [N] (or [N, N]) the slot noise levels; prefix_k/v [L, P_max, Hkv, dh] the
+    one shared observation.  Every configuration attends to the same prefix
+    and is isolated from the others, so the packed forward is the velocity of
+    each configuration with its own padding.  Returns v [N, N, C, A]; entries
+    of padding slots are the padding queries' outputs (never used).
+    """
+    N = buffers.shape[0]
+    t = np.broadcast_to(np.asarray(t, np.float32), (N, N))
+    return np.stack([velocity(buffers[j], t[j], prefix_k, prefix_v, prefix_len, w, cfg, dtype,
+                              mask=mask, first_valid=N - 1 - j) for j in range(N)])
+
+
 def sequential_levels(n_steps: int) -> np.ndarray:
     """Sequential decode schedule t_j = fl32((n - j)/n), j = 0..n (t_n = 0)."""
     return (np.arange(n_steps, -1, -1, dtype=np.float64) / n_steps).astype(np.float32)

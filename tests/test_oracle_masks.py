@@ -185,3 +185,53 @@ def test_cold_start_leaves_other_streams_alone():
     new = oracle.cold_start(x, [1], 0, 0)
     assert np.array_equal(new[0], x[0]) and np.array_equal(new[2], x[2])
     assert not np.array_equal(new[1], x[1])
+
+
+def test_packed_multibuffer_attention_equals_isolated_configurations():
+    """Sec. 3.3 packs all N buffer configurations of one observation into one
+    sequence whose attention mask isolates the configurations.  A dense
+    attention over that packed sequence (mask written out token by token)
+    equals the per-configuration attention with padding used by the
+    multi-buffer forward."""
+    rng = np.random.default_rng(7)
+    N, C, P, Hq, Hkv, dh = 3, 2, 4, 2, 1, 8
+    T = N * C
+    q = rng.standard_normal((N, T, Hq, dh))
+    kb, vb = rng.standard_normal((N, T, Hkv, dh)), rng.standard_normal((N, T, Hkv, dh))
+    kp, vp = rng.standard_normal((P, Hkv, dh)), rng.standard_normal((P, Hkv, dh))
+    # packed sequence: [prefix ; config 1 tokens ; ... ; config N tokens]
+    keys = np.concatenate([kp] + [kb[j] for j in range(N)])
+    vals = np.concatenate([vp] + [vb[j] for j in range(N)])
+    out_packed = np.zeros((N, T, Hq, dh))
+    for j in range(N):
+        first = N - 1 - j                      # configuration j+1 has j+1 real chunks
+        for i in range(T):
+            vis = np.zeros(P + N * T, bool)
+            vis[:P] = True
+            for jj in range(N):
+                for tk in range(T):
+                    if jj == j:                # other configurations are invisible
+                        vis[P + jj * T + tk] = _rule(i // C, tk // C, first, "causal")
+            for h in range(Hq):
+                g = h // (Hq // Hkv)
+                sc = np.where(vis, keys[:, g] @ q[j, i, h] / math.sqrt(dh), -np.inf)
+                out_packed[j, i, h] = special.softmax(sc) @ vals[:, g]
+    for j in range(N):
+        o = oracle.chunk_causal_attention(q[j], kb[j], vb[j], kp, vp, C, first_valid=N - 1 - j)
+        np.testing.assert_allclose(o, out_packed[j], rtol=0, atol=1e-12)
+
+
+def test_multibuffer_forward_is_the_cold_start_sequence_of_buffer_states():
+    """Configuration j of the packed forward is exactly the buffer state a
+    cold-started stream has after j-1 steps (same padding, same slots)."""
+    W, k, v, P, x, t = _setup(5)
+    N = PIN.n_chunks
+    bufs = np.stack([x.copy() for _ in range(N)])
+    for j in range(N):
+        bufs[j, :N - 1 - j] = 0.0
+    got = oracle.multibuffer_velocity(bufs, t, k, v, P, W, PIN)
+    for j in range(N):
+        ref = oracle.velocity(bufs[j], t, k, v, P, W, PIN, first_valid=N - 1 - j)
+        assert np.array_equal(got[j], ref)
+    # the full configuration is the steady-state buffer
+    assert np.array_equal(got[N - 1], oracle.velocity(x, t, k, v, P, W, PIN))
