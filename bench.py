@@ -136,25 +136,40 @@ def pct(xs, q):
     return float(np.percentile(np.asarray(xs), q))
 
 
-def measure_streaming(w, steps, warmup, with_roofline):
+def film_bytes(w) -> int:
+    """Bytes of the time-MLP and FiLM map weights (skipped by a cached schedule)."""
+    e = 2 if w.dtype == synth.BF16 else 4
+    W, L = w.width, w.n_layers
+    return (2 * W * W + (6 * L + 2) * W * W) * e + (2 * W + (6 * L + 2) * W) * 4
+
+
+def measure_streaming(w, steps, warmup, with_roofline, cached=False, mask=None):
+    """Steady streaming steps.  cached: static-schedule FiLM cache (t == NULL);
+    mask: attention mask mode name (default chunk-causal)."""
     import torch
     from paper_2608_27384_amd.flashvla import Expert
     inp = Inputs(w)
     ex = Expert(inp.W, w, w.batch, w.max_prefix, noise_seed=w.noise_seed)
     try:
         ex.set_prefix(inp.kd, inp.vd, inp.lens)
+        if mask:
+            ex.set_mask_mode(mask)
         xd = torch.from_numpy(inp.x).cuda()
         td = torch.from_numpy(inp.t).cuda()
         out = torch.empty((w.batch, w.chunk_len, w.action_dim), dtype=torch.float32,
                           device="cuda")
-        per, total_ms, wall = time_steps(lambda: ex.decode_step(xd, td, out), steps, warmup)
+        if cached:
+            ex.set_schedule(td)
+        tt = None if cached else td
+        per, total_ms, wall = time_steps(lambda: ex.decode_step(xd, tt, out), steps, warmup)
         assert bool(torch.isfinite(out).all()) and bool(torch.isfinite(xd).all()), \
             "non-finite decode output"
         ms = total_ms / steps
         gemm_f, attn_f = step_flops(w, inp.lens)
-        nbytes = step_bytes(w, inp.lens)
+        nbytes = step_bytes(w, inp.lens) - (film_bytes(w) if cached else 0)
         res = {
             "workload": w.name, "batch": w.batch, "n_chunks": w.n_chunks,
+            "variant": ("static-schedule cache; " if cached else "") + f"mask {mask or 'causal'}",
             "chunk_len": w.chunk_len, "action_dim": w.action_dim,
             "prefix_len": [int(inp.lens.min()), int(inp.lens.max())],
             "steps": steps, "warmup": warmup, "ms_per_step": ms,
@@ -239,6 +254,76 @@ def stage_rooflines(ex, w, lens):
                      "hbm_frac": nbytes / (ms / 1e3) / (HBM_PEAK_GBS * 1e9),
                      "flops": flops, "bytes": nbytes}
     return out
+
+
+def measure_cold_start(w, episodes=20):
+    """Episode start: fv_cold_start, then K steps until the first real chunk is
+    emitted (the K-1 warm-up steps emit zeros).  HIP events on the stream."""
+    import torch
+    from paper_2608_27384_amd.flashvla import Expert
+    inp = Inputs(w)
+    ex = Expert(inp.W, w, w.batch, w.max_prefix, noise_seed=w.noise_seed)
+    try:
+        ex.set_prefix(inp.kd, inp.vd, inp.lens)
+        xd = torch.from_numpy(inp.x).cuda()
+        td = torch.from_numpy(inp.t).cuda()
+        out = torch.empty((w.batch, w.chunk_len, w.action_dim), dtype=torch.float32,
+                          device="cuda")
+
+        def episode():
+            ex.cold_start(xd)
+            for _ in range(w.n_chunks):
+                ex.decode_step(xd, td, out)
+
+        episode()
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(out).all()) and float(out.abs().max()) > 0.0
+        st, en = _events(episodes), _events(episodes)
+        cs_ms = []
+        for i in range(episodes):
+            a = _events(1)[0]
+            st[i].record()
+            ex.cold_start(xd)
+            a.record()
+            for _ in range(w.n_chunks):
+                ex.decode_step(xd, td, out)
+            en[i].record()
+            cs_ms.append((st[i], a))
+        torch.cuda.synchronize()
+        tta = [s_.elapsed_time(e_) for s_, e_ in zip(st, en)]
+        cs = [s_.elapsed_time(e_) for s_, e_ in cs_ms]
+        return {"workload": w.name, "episodes": episodes, "warmup_steps": w.n_chunks - 1,
+                "cold_start_call_us": pct(cs, 50) * 1e3,
+                "time_to_first_action_ms_p50": pct(tta, 50),
+                "time_to_first_action_ms_p99": pct(tta, 99)}
+    finally:
+        ex.close()
+
+
+def measure_multibuffer(w, reps=50, warmup=5):
+    """Packed multi-buffer forward of one observation (Sec. 3.3): the K buffer
+    configurations of cold start in one call."""
+    import torch
+    from paper_2608_27384_amd.flashvla import Expert
+    inp = Inputs(w)
+    K = w.n_chunks
+    ex = Expert(inp.W, w, max(w.batch, K), w.max_prefix, noise_seed=w.noise_seed)
+    try:
+        bufs = np.stack([inp.x[0].copy() for _ in range(K)])
+        for j in range(K):
+            bufs[j, :K - 1 - j] = 0.0
+        bd = torch.from_numpy(bufs).cuda()
+        tdv = torch.from_numpy(np.broadcast_to(inp.t[0], (K, K)).copy()).cuda()
+        kd, vd = inp.kd[:, 0].contiguous(), inp.vd[:, 0].contiguous()
+        vout = torch.empty_like(bd)
+        per, total_ms, _ = time_steps(
+            lambda: ex.multibuffer_velocity(kd, vd, int(inp.lens[0]), bd, tdv, vout), reps, warmup)
+        assert bool(torch.isfinite(vout[:, -1]).all())
+        return {"workload": w.name, "configurations": K, "reps": reps,
+                "ms_per_call": total_ms / reps, "p50_us": pct(per, 50) * 1e3,
+                "note": "includes installing the shared prefix for all configurations"}
+    finally:
+        ex.close()
 
 
 def measure_sequential(w, chunks, warmup):
@@ -357,6 +442,19 @@ def main():
                       file=sys.stderr, flush=True)
         others["seq_baseline"] = measure_sequential(synth.workload("seq_baseline"), 100, 10)
         print(f"# seq_baseline: {others['seq_baseline']['ms_per_chunk'] * 1e3:.1f} us/chunk",
+              file=sys.stderr, flush=True)
+        for key, kw in (("pi05_b1_static_schedule", {"cached": True}),
+                        ("pi05_b1_isolated_mask", {"mask": "isolated"})):
+            others[key] = measure_streaming(synth.workload("pi05_b1"), 100, 10, False, **kw)
+            print(f"# {key}: {others[key]['ms_per_step'] * 1e3:.1f} us/step",
+                  file=sys.stderr, flush=True)
+        others["pi05_b1_multibuffer"] = measure_multibuffer(synth.workload("pi05_b1"))
+        print(f"# pi05_b1 multi-buffer forward: "
+              f"{others['pi05_b1_multibuffer']['ms_per_call'] * 1e3:.1f} us/call",
+              file=sys.stderr, flush=True)
+        others["pi05_b1_cold_start"] = measure_cold_start(synth.workload("pi05_b1"))
+        print(f"# pi05_b1 cold start: first action after "
+              f"{others['pi05_b1_cold_start']['time_to_first_action_ms_p50']:.2f} ms",
               file=sys.stderr, flush=True)
 
     stages = main_res.pop("stages")

@@ -256,6 +256,37 @@ fv_status fv_cold_start(fv_handle h, float *buffer, int32_t first_stream, int32_
 fv_status fv_get_valid_slots(fv_handle h, int32_t *out, int32_t count);
 
 /*
+ * fv_set_valid_slots -- set the valid (non-padding) slot count of the first
+ * `count` streams from host int32 n_valid[count] (each 1..K; the last
+ * n_valid slots of a stream are real chunks).  Restores a saved cold-start
+ * state; fv_cold_start and fv_decode_step maintain the counts otherwise.
+ * Synchronises the device.
+ * Errors: FV_ERR_INVALID_ARG (NULL, count outside 1..max_batch, a count
+ * outside 1..K).
+ */
+fv_status fv_set_valid_slots(fv_handle h, const int32_t *n_valid, int32_t count);
+
+/*
+ * fv_multibuffer_velocity -- forward pass of the packed multi-buffer sample
+ * of Sec. 3.3 for one observation: the N = K buffer configurations that cold
+ * start passes through, configuration j (j = 1..N) holding N - j padding
+ * chunks followed by j real chunks, all attending to the same observation
+ * and isolated from each other.  Configuration j runs as stream j - 1.
+ *  k, v       dev [L][ld][Hkv][dh] (cfg dtype): the one observation prefix,
+ *             installed for all N streams (prefix_len rows valid).
+ *  buffers    dev fp32 [N][K][C][A]: configuration j at index j - 1.
+ *  t          dev fp32 [N][K]: slot noise levels of every configuration.
+ *  v_out      dev fp32 [N][K][C][A]: velocities (padding slots: unused values).
+ * Leaves the handle with batch N, that prefix, and valid slot counts
+ * 1..N.  Needs max_batch >= K.  Host-synchronous for the prefix install.
+ * Errors: FV_ERR_INVALID_ARG (pointers, prefix_len, ld, max_batch < K),
+ * FV_ERR_HIP.
+ */
+fv_status fv_multibuffer_velocity(fv_handle h, const void *k, const void *v, int32_t prefix_len,
+                                  int32_t ld, const float *buffers, const float *t, float *v_out,
+                                  void *stream);
+
+/*
  * fv_set_graph_mode -- 1 (default): each step is one hipGraphLaunch of a
  * captured graph; 0: kernels are launched one by one on the caller's stream
  * (same kernels, same results).  Errors: FV_ERR_INVALID_ARG.

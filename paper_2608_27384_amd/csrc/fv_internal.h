@@ -163,8 +163,9 @@ void launch_cold_start(float* buffer, uint64_t* noise_state, int* n_valid, int b
 void launch_copy_f32(float* dst, const float* src, size_t n, hipStream_t s);
 void launch_fill_t(float* t, const float* tsched, int j, int B, hipStream_t s);
 template <typename T>
-void launch_prefix_copy(const T* k, const T* v, int L, int B, int ld, int Hkv, int dh,
-                        T* karena, T* vtarena, int Bmax, int S, const int* len, hipStream_t s);
+void launch_prefix_copy(const T* k, const T* v, int L, int B, int src_batch, int ld, int Hkv,
+                        int dh, T* karena, T* vtarena, int Bmax, int S, const int* len,
+                        hipStream_t s);
 
 struct AttnArgs {
   const void* q;        // [B*tokens][Hq][dh]

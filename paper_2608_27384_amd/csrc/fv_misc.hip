@@ -451,7 +451,7 @@ __global__ void fill_t_kernel(float* __restrict__ t, const float* __restrict__ t
 template <typename T>
 __global__ __launch_bounds__(256) void prefix_copy_kernel(const T* __restrict__ k,
                                                           const T* __restrict__ v, int B,
-                                                          int ld, int Hkv, int dh,
+                                                          int src_batch, int ld, int Hkv, int dh,
                                                           T* __restrict__ karena,
                                                           T* __restrict__ vtarena, int Bmax,
                                                           int S, const int* __restrict__ len) {
@@ -462,7 +462,8 @@ __global__ __launch_bounds__(256) void prefix_copy_kernel(const T* __restrict__ 
   const int n = len[b];
   const int p0 = pt * 64, d0 = dt * 64;
   if (p0 >= n) return;
-  const size_t src_base = (((size_t)l * B + b) * ld) * Hkv * dh;
+  // src_batch == 1: one observation shared by every stream
+  const size_t src_base = (((size_t)l * src_batch + (src_batch == 1 ? 0 : b)) * ld) * Hkv * dh;
   const size_t kdst = (((size_t)l * Bmax + b) * Hkv + g) * (size_t)S * dh;
   const size_t vdst = (((size_t)l * Bmax + b) * Hkv + g) * (size_t)dh * S;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
@@ -558,11 +559,12 @@ void launch_fill_t(float* t, const float* tsched, int j, int B, hipStream_t s) {
 }
 
 template <typename T>
-void launch_prefix_copy(const T* k, const T* v, int L, int B, int ld, int Hkv, int dh,
-                        T* karena, T* vtarena, int Bmax, int S, const int* len, hipStream_t s) {
+void launch_prefix_copy(const T* k, const T* v, int L, int B, int src_batch, int ld, int Hkv,
+                        int dh, T* karena, T* vtarena, int Bmax, int S, const int* len,
+                        hipStream_t s) {
   dim3 grid((ld + 63) / 64, (dh + 63) / 64, L * B * Hkv);
-  hipLaunchKernelGGL((prefix_copy_kernel<T>), grid, dim3(256), 0, s, k, v, B, ld, Hkv, dh,
-                     karena, vtarena, Bmax, S, len);
+  hipLaunchKernelGGL((prefix_copy_kernel<T>), grid, dim3(256), 0, s, k, v, B, src_batch, ld, Hkv,
+                     dh, karena, vtarena, Bmax, S, len);
 }
 
 template void launch_time_embed<bf16_t>(const float*, bf16_t*, int, int, hipStream_t);
@@ -582,8 +584,8 @@ template void launch_adarms<bf16_t>(const float*, const float*, int, int, int, f
 template void launch_adarms<float>(const float*, const float*, int, int, int, float, float*, int,
                                    int, hipStream_t);
 template void launch_prefix_copy<bf16_t>(const bf16_t*, const bf16_t*, int, int, int, int, int,
-                                         bf16_t*, bf16_t*, int, int, const int*, hipStream_t);
-template void launch_prefix_copy<float>(const float*, const float*, int, int, int, int, int,
+                                         int, bf16_t*, bf16_t*, int, int, const int*, hipStream_t);
+template void launch_prefix_copy<float>(const float*, const float*, int, int, int, int, int, int,
                                         float*, float*, int, int, const int*, hipStream_t);
 
 }  // namespace fv

@@ -633,13 +633,13 @@ fv_status fv_set_prefix(fv_handle h, const void* k, const void* v, const int32_t
     FV_HIP(hipMemcpyAsync(h->d_len, h->len_host.data(), (size_t)batch * 4, hipMemcpyHostToDevice, s));
     if (ld > 0 && maxlen > 0) {
       if (h->bf16)
-        launch_prefix_copy<bf16_t>((const bf16_t*)k, (const bf16_t*)v, h->L, batch, ld, h->Hkv,
-                                   h->dh, (bf16_t*)h->karena, (bf16_t*)h->vtarena, h->Bmax, h->S,
-                                   h->d_len, s);
+        launch_prefix_copy<bf16_t>((const bf16_t*)k, (const bf16_t*)v, h->L, batch, batch, ld,
+                                   h->Hkv, h->dh, (bf16_t*)h->karena, (bf16_t*)h->vtarena,
+                                   h->Bmax, h->S, h->d_len, s);
       else
-        launch_prefix_copy<float>((const float*)k, (const float*)v, h->L, batch, ld, h->Hkv, h->dh,
-                                  (float*)h->karena, (float*)h->vtarena, h->Bmax, h->S, h->d_len,
-                                  s);
+        launch_prefix_copy<float>((const float*)k, (const float*)v, h->L, batch, batch, ld, h->Hkv,
+                                  h->dh, (float*)h->karena, (float*)h->vtarena, h->Bmax, h->S,
+                                  h->d_len, s);
       check_launch();
     }
     // The host copy of len must stay valid until the async copy has read it.
@@ -740,6 +740,63 @@ fv_status fv_sequential_decode(fv_handle h, const float* noise, int32_t n_steps,
                }
                launch_copy_f32(out_chunk, h->seq_x, n, s);
              });
+  });
+}
+
+fv_status fv_set_valid_slots(fv_handle h, const int32_t* n_valid, int32_t count) {
+  if (!h) return FV_ERR_INVALID_ARG;
+  return guarded(h, [&] {
+    need(n_valid, "n_valid");
+    if (count < 1 || count > h->Bmax) fail(FV_ERR_INVALID_ARG, "count outside 1..max_batch");
+    for (int b = 0; b < count; ++b)
+      if (n_valid[b] < 1 || n_valid[b] > h->K)
+        fail(FV_ERR_INVALID_ARG, "valid slot count outside 1..n_chunks");
+    DeviceScope ds(h->device);
+    FV_HIP(hipDeviceSynchronize());
+    FV_HIP(hipMemcpy(h->d_valid, n_valid, (size_t)count * 4, hipMemcpyHostToDevice));
+  });
+}
+
+fv_status fv_multibuffer_velocity(fv_handle h, const void* k, const void* v, int32_t prefix_len,
+                                  int32_t ld, const float* buffers, const float* t, float* v_out,
+                                  void* stream) {
+  if (!h) return FV_ERR_INVALID_ARG;
+  return guarded(h, [&] {
+    need(k, "k");
+    need(v, "v");
+    check_ptr(buffers, "buffers");
+    check_ptr(t, "t");
+    check_ptr(v_out, "v_out");
+    const int N = h->K;
+    if (h->Bmax < N) fail(FV_ERR_INVALID_ARG, "max_batch must be >= n_chunks");
+    if (prefix_len < 0 || prefix_len > h->Pmax) fail(FV_ERR_INVALID_ARG, "prefix_len out of range");
+    if (ld < prefix_len) fail(FV_ERR_INVALID_ARG, "ld must be >= prefix_len");
+    DeviceScope ds(h->device);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    // one observation for all N configurations; configuration j (stream j-1)
+    // holds j real chunks after N - j padding slots
+    h->len_host.assign(N, prefix_len);
+    std::vector<int> valid(N);
+    for (int j = 0; j < N; ++j) valid[j] = j + 1;
+    FV_HIP(hipMemcpyAsync(h->d_len, h->len_host.data(), (size_t)N * 4, hipMemcpyHostToDevice, s));
+    FV_HIP(hipMemcpyAsync(h->d_valid, valid.data(), (size_t)N * 4, hipMemcpyHostToDevice, s));
+    if (ld > 0 && prefix_len > 0) {
+      if (h->bf16)
+        launch_prefix_copy<bf16_t>((const bf16_t*)k, (const bf16_t*)v, h->L, N, 1, ld, h->Hkv,
+                                   h->dh, (bf16_t*)h->karena, (bf16_t*)h->vtarena, h->Bmax, h->S,
+                                   h->d_len, s);
+      else
+        launch_prefix_copy<float>((const float*)k, (const float*)v, h->L, N, 1, ld, h->Hkv, h->dh,
+                                  (float*)h->karena, (float*)h->vtarena, h->Bmax, h->S, h->d_len,
+                                  s);
+      check_launch();
+    }
+    FV_HIP(hipStreamSynchronize(s));  // the host copies above must stay valid until read
+    h->batch = N;
+    h->prefix_set = true;
+    run_step(h, KIND_VELOCITY, buffers, t, v_out, nullptr, 0, s,
+             [&](hipStream_t st) { forward(h, buffers, t, N, v_out, h->L, st); });
   });
 }
 

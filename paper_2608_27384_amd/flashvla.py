@@ -29,7 +29,7 @@ EXPORTED = (
     "fv_sequential_decode", "fv_get_noise_state", "fv_set_noise_state", "fv_set_graph_mode",
     "fv_destroy", "fv_status_string", "fv_last_error", "fv_abi_version", "fv_debug_forward",
     "fv_debug_stage", "fv_query", "fv_set_mask_mode", "fv_set_schedule", "fv_cold_start",
-    "fv_get_valid_slots",
+    "fv_get_valid_slots", "fv_set_valid_slots", "fv_multibuffer_velocity",
 )
 
 
@@ -85,6 +85,9 @@ def lib() -> ctypes.CDLL:
             "fv_set_schedule": ([H, c_void_p, c_void_p], S),
             "fv_cold_start": ([H, c_void_p, c_int32, c_int32, c_void_p], S),
             "fv_get_valid_slots": ([H, POINTER(c_int32), c_int32], S),
+            "fv_set_valid_slots": ([H, POINTER(c_int32), c_int32], S),
+            "fv_multibuffer_velocity": ([H, c_void_p, c_void_p, c_int32, c_int32, c_void_p,
+                                         c_void_p, c_void_p, c_void_p], S),
         }
         for name, (args, res) in sig.items():
             fn = getattr(L, name)
@@ -228,6 +231,18 @@ def fv_get_valid_slots(h, count: int):
     return [int(x) for x in arr]
 
 
+def fv_set_valid_slots(h, counts: Sequence[int]) -> None:
+    arr = (c_int32 * len(counts))(*[int(c) for c in counts])
+    _check(h, lib().fv_set_valid_slots(h, arr, len(counts)), "fv_set_valid_slots")
+
+
+def fv_multibuffer_velocity(h, k, v, prefix_len: int, ld: int, buffers, t, v_out,
+                            stream=None) -> None:
+    _check(h, lib().fv_multibuffer_velocity(h, _ptr(k), _ptr(v), prefix_len, ld, _ptr(buffers),
+                                            _ptr(t), _ptr(v_out), _stream(stream)),
+           "fv_multibuffer_velocity")
+
+
 def fv_query(h, what: int, batch: int = 1) -> int:
     val = c_int64(0)
     _check(h, lib().fv_query(h, what, batch, ctypes.byref(val)), "fv_query")
@@ -293,6 +308,14 @@ class Expert:
     def cold_start(self, buffer, first_stream=0, n_streams=None, stream=None):
         n = self.batch - first_stream if n_streams is None else n_streams
         fv_cold_start(self.handle, buffer, first_stream, n, stream)
+
+    def set_valid_slots(self, counts):
+        fv_set_valid_slots(self.handle, counts)
+
+    def multibuffer_velocity(self, k, v, prefix_len, buffers, t, v_out, stream=None):
+        fv_multibuffer_velocity(self.handle, k, v, prefix_len, k.shape[1], buffers, t, v_out,
+                                stream)
+        self.batch = self.cfg.n_chunks
 
     def valid_slots(self, count=None):
         return fv_get_valid_slots(self.handle, self.batch if count is None else count)
