@@ -326,6 +326,65 @@ def measure_multibuffer(w, reps=50, warmup=5):
         ex.close()
 
 
+def measure_async_pipeline(w, steps=60, warmup=6, hz=30.0):
+    """Control loop with a new observation every step (the VLM prefix forward
+    itself is not part of this library): either the prefix is installed and
+    then the step runs on one stream (serialized), or the next observation is
+    installed on a second stream while the current step runs (overlapped,
+    fv_set_prefix_async).  Also reports the time-to-first-action /
+    time-to-react model of Sec. 4.3 for a 30 Hz executor that runs the
+    emitted chunk (C actions): TTR = TTFA + 0.5 * C / hz."""
+    import torch
+    from paper_2608_27384_amd.flashvla import Expert
+    inp = Inputs(w)
+    obs = []
+    for i in range(2):
+        k, v, lens = synth.make_prefix(w, seed=200 + i)
+        if w.dtype == synth.BF16:
+            kd = torch.from_numpy(synth.bf16_bits(k).view(np.int16)).cuda()
+            vd = torch.from_numpy(synth.bf16_bits(v).view(np.int16)).cuda()
+        else:
+            kd, vd = torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda()
+        obs.append((kd, vd, [int(x) for x in lens]))
+    res = {"workload": w.name, "batch": w.batch, "steps": steps}
+    for mode in ("serialized", "overlapped"):
+        ex = Expert(inp.W, w, w.batch, w.max_prefix, noise_seed=w.noise_seed)
+        try:
+            xd = torch.from_numpy(inp.x).cuda()
+            td = torch.from_numpy(inp.t).cuda()
+            out = torch.empty((w.batch, w.chunk_len, w.action_dim), dtype=torch.float32,
+                              device="cuda")
+            cs = torch.cuda.Stream()
+            kd, vd, lens = obs[0]
+            ex.set_prefix(kd, vd, lens)
+            state = {"i": 0}
+
+            def control_step():
+                i = state["i"]
+                state["i"] += 1
+                kd, vd, lens = obs[(i + 1) % 2]
+                if mode == "serialized":
+                    ex.decode_step(xd, td, out)
+                    ex.set_prefix(kd, vd, lens)      # next observation, same stream
+                else:
+                    ex.decode_step(xd, td, out)
+                    ex.set_prefix_async(kd, vd, lens, cs)
+
+            per, total_ms, wall = time_steps(control_step, steps, warmup)
+            torch.cuda.synchronize()
+            res[mode] = {"ms_per_control_step": wall * 1e3 / steps, "p50_us": pct(per, 50) * 1e3}
+        finally:
+            ex.close()
+    ttfa = res["overlapped"]["ms_per_control_step"]
+    exec_ms = 1e3 * w.chunk_len / hz
+    res["ttfa_ms"] = ttfa
+    res["ttr_expected_ms"] = ttfa + 0.5 * exec_ms
+    res["executor_hz"] = hz
+    res["note"] = ("per control step: decode step + install of the next observation's prefix; "
+                   "wall clock per step including host calls (serialized waits for each install)")
+    return res
+
+
 def measure_sequential(w, chunks, warmup):
     import torch
     from paper_2608_27384_amd.flashvla import Expert
@@ -452,6 +511,12 @@ def main():
         print(f"# pi05_b1 multi-buffer forward: "
               f"{others['pi05_b1_multibuffer']['ms_per_call'] * 1e3:.1f} us/call",
               file=sys.stderr, flush=True)
+        for name in ("pi05_b1", "batched64"):
+            key = f"{name}_async_pipeline"
+            others[key] = measure_async_pipeline(synth.workload(name))
+            print(f"# {key}: serialized {others[key]['serialized']['ms_per_control_step']:.3f} ms, "
+                  f"overlapped {others[key]['overlapped']['ms_per_control_step']:.3f} ms",
+                  file=sys.stderr, flush=True)
         others["pi05_b1_cold_start"] = measure_cold_start(synth.workload("pi05_b1"))
         print(f"# pi05_b1 cold start: first action after "
               f"{others['pi05_b1_cold_start']['time_to_first_action_ms_p50']:.2f} ms",

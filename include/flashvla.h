@@ -145,6 +145,24 @@ fv_status fv_set_prefix(fv_handle h, const void *k, const void *v, const int32_t
                         int32_t batch, int32_t ld, void *stream);
 
 /*
+ * fv_set_prefix_async -- asynchronous observation pipeline: install the
+ * prefix of the next observation while the current one is still being
+ * decoded (Sec. 4.2: the next inference starts before the current chunk has
+ * finished executing).  Same arguments as fv_set_prefix, enqueued on
+ * `copy_stream`.  The data go to a second arena slot (allocated by the first
+ * call: as much device memory as the first arena), so passes still running
+ * on the active observation are unaffected; the next fv_decode_step /
+ * fv_velocity / fv_sequential_decode / fv_debug_forward makes its stream
+ * wait for this copy and switches to the new observation (and its batch).
+ * No host synchronisation except on a slot's third reuse before its previous
+ * length copy finished.  A later fv_set_prefix_async before that switch
+ * replaces the pending observation; fv_set_prefix cancels it.
+ * Errors: FV_ERR_INVALID_ARG (as fv_set_prefix), FV_ERR_OOM, FV_ERR_HIP.
+ */
+fv_status fv_set_prefix_async(fv_handle h, const void *k, const void *v, const int32_t *len_host,
+                              int32_t batch, int32_t ld, void *copy_stream);
+
+/*
  * fv_decode_step -- one streaming step (Algorithm 1).
  *  buffer       dev fp32 [batch][K][C][A], in/out.  Slot 0 is the cleanest chunk.
  *  t_per_chunk  dev fp32 [batch][K]: noise level of each slot (0 < t_0 < ... ),

@@ -203,7 +203,7 @@ int attention_row_tiles(int tokens, int n_q_heads, int n_kv_heads);
 
 // ------------------------------------------------------------------- handle
 struct GraphEntry {
-  int kind = 0, batch = 0, n = 0;
+  int kind = 0, batch = 0, n = 0, slot = 0;
   const void* p[4] = {nullptr, nullptr, nullptr, nullptr};
   hipGraphExec_t exec = nullptr;
   uint64_t last_use = 0;
@@ -253,6 +253,20 @@ struct Handle {
   GemmWork gw;                    // split-K workspace and counters
   uint64_t* d_noise = nullptr;   // {seed, step}
   int* d_valid = nullptr;        // [Bmax] non-padding slots per stream (K: steady state)
+  // Double-buffered observation prefix for the asynchronous pipeline: slot
+  // cur_slot is the active arena (karena / vtarena / d_len point at it);
+  // fv_set_prefix_async fills the other slot on the caller's copy stream.
+  void* arena_k[2] = {nullptr, nullptr};
+  void* arena_v[2] = {nullptr, nullptr};
+  int* len_slot[2] = {nullptr, nullptr};
+  std::vector<int> len_host_slot[2];
+  int cur_slot = 0, staged_slot = -1, staged_batch = 0;
+  bool async_ready = false;                    // second slot and events exist
+  hipEvent_t ev_ready[2] = {nullptr, nullptr}; // staged prefix copied (copy stream)
+  hipEvent_t ev_done[2] = {nullptr, nullptr};  // last pass that read the slot
+  hipEvent_t ev_len[2] = {nullptr, nullptr};   // pinned length buffer consumed
+  bool done_recorded[2] = {false, false}, len_recorded[2] = {false, false};
+  int* pinned_len[2] = {nullptr, nullptr};
   int mask_mode = FV_MASK_CHUNK_CAUSAL;
   float* mod_cache = nullptr;    // [Bmax*K][Nmod] FiLM maps of a static schedule
   float* t_cache = nullptr;      // [Bmax*K] the schedule itself

@@ -311,8 +311,8 @@ void run_step(Handle* h, int kind, const void* p0, const void* p1, const void* p
   }
   GraphEntry* ent = nullptr;
   for (GraphEntry& g : h->graphs)
-    if (g.kind == kind && g.batch == h->batch && g.n == n && g.p[0] == p0 && g.p[1] == p1 &&
-        g.p[2] == p2 && g.p[3] == p3)
+    if (g.kind == kind && g.batch == h->batch && g.n == n && g.slot == h->cur_slot &&
+        g.p[0] == p0 && g.p[1] == p1 && g.p[2] == p2 && g.p[3] == p3)
       ent = &g;
   if (!ent) {
     if (h->graphs.size() >= 8) {
@@ -346,6 +346,7 @@ void run_step(Handle* h, int kind, const void* p0, const void* p1, const void* p
     g.kind = kind;
     g.batch = h->batch;
     g.n = n;
+    g.slot = h->cur_slot;
     g.p[0] = p0; g.p[1] = p1; g.p[2] = p2; g.p[3] = p3;
     g.exec = exec;
     h->graphs.push_back(g);
@@ -368,7 +369,8 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb) {
 }
 
 void need_prefix(const Handle* h) {
-  if (!h->prefix_set) fail(FV_ERR_STATE, "no observation prefix: call fv_set_prefix first");
+  if (!h->prefix_set && h->staged_slot < 0)
+    fail(FV_ERR_STATE, "no observation prefix: call fv_set_prefix first");
 }
 
 enum Kind { KIND_STEP = 1, KIND_VELOCITY = 2, KIND_SEQ = 3, KIND_STEP_CACHED = 4,
@@ -400,8 +402,39 @@ void destroy_handle(Handle* h) {
   h->graphs.clear();
   for (void* p : h->allocations) (void)hipFree(p);
   h->allocations.clear();
+  for (int i = 0; i < 2; ++i) {
+    if (h->pinned_len[i]) (void)hipHostFree(h->pinned_len[i]);
+    if (h->ev_ready[i]) (void)hipEventDestroy(h->ev_ready[i]);
+    if (h->ev_done[i]) (void)hipEventDestroy(h->ev_done[i]);
+    if (h->ev_len[i]) (void)hipEventDestroy(h->ev_len[i]);
+    h->pinned_len[i] = nullptr;
+    h->ev_ready[i] = h->ev_done[i] = h->ev_len[i] = nullptr;
+  }
   if (h->cap_stream) (void)hipStreamDestroy(h->cap_stream);
   h->cap_stream = nullptr;
+}
+
+// A pass about to read the prefix on `stream`: switch to a staged
+// observation (the stream waits for its copy) ...
+void activate_staged(Handle* h, hipStream_t stream) {
+  if (h->staged_slot < 0) return;
+  const int sl = h->staged_slot;
+  FV_HIP(hipStreamWaitEvent(stream, h->ev_ready[sl], 0));
+  h->cur_slot = sl;
+  h->karena = h->arena_k[sl];
+  h->vtarena = h->arena_v[sl];
+  h->d_len = h->len_slot[sl];
+  h->len_host = h->len_host_slot[sl];
+  h->batch = h->staged_batch;
+  h->staged_slot = -1;
+  h->prefix_set = true;
+}
+
+// ... and after it: the slot is free for restaging once `stream` passes here.
+void mark_used(Handle* h, hipStream_t stream) {
+  if (!h->async_ready) return;
+  FV_HIP(hipEventRecord(h->ev_done[h->cur_slot], stream));
+  h->done_recorded[h->cur_slot] = true;
 }
 
 }  // namespace
@@ -556,6 +589,9 @@ fv_status fv_create(const fv_weights* w, const fv_cfg* cfg, fv_handle* out) {
     FV_HIP(hipMemset(H.vtarena, 0, arena));
     H.d_len = static_cast<int*>(dalloc(h, (size_t)H.Bmax * 4));
     FV_HIP(hipMemset(H.d_len, 0, (size_t)H.Bmax * 4));
+    H.arena_k[0] = H.karena;
+    H.arena_v[0] = H.vtarena;
+    H.len_slot[0] = H.d_len;
     {
       const std::vector<int> full(H.Bmax, H.K);  // every stream starts in steady state
       H.d_valid = static_cast<int*>(dalloc(h, (size_t)H.Bmax * 4));
@@ -629,6 +665,7 @@ fv_status fv_set_prefix(fv_handle h, const void* k, const void* v, const int32_t
     if (ld < maxlen || ld < 0) fail(FV_ERR_INVALID_ARG, "ld must be >= max(len)");
     DeviceScope ds(h->device);
     hipStream_t s = static_cast<hipStream_t>(stream);
+    h->staged_slot = -1;  // a pending asynchronous observation is superseded
     h->len_host.assign(len_host, len_host + batch);
     FV_HIP(hipMemcpyAsync(h->d_len, h->len_host.data(), (size_t)batch * 4, hipMemcpyHostToDevice, s));
     if (ld > 0 && maxlen > 0) {
@@ -649,6 +686,70 @@ fv_status fv_set_prefix(fv_handle h, const void* k, const void* v, const int32_t
   });
 }
 
+fv_status fv_set_prefix_async(fv_handle h, const void* k, const void* v, const int32_t* len_host,
+                              int32_t batch, int32_t ld, void* copy_stream) {
+  if (!h) return FV_ERR_INVALID_ARG;
+  return guarded(h, [&] {
+    need(k, "k");
+    need(v, "v");
+    need(len_host, "len_host");
+    if (batch < 1 || batch > h->Bmax)
+      fail(FV_ERR_INVALID_ARG, "batch must be in [1, max_batch=" + std::to_string(h->Bmax) + "]");
+    int maxlen = 0;
+    for (int b = 0; b < batch; ++b) {
+      if (len_host[b] < 0 || len_host[b] > h->Pmax)
+        fail(FV_ERR_INVALID_ARG, "len[" + std::to_string(b) + "] outside [0, max_prefix]");
+      maxlen = std::max(maxlen, (int)len_host[b]);
+    }
+    if (ld < maxlen || ld < 0) fail(FV_ERR_INVALID_ARG, "ld must be >= max(len)");
+    DeviceScope ds(h->device);
+    if (!h->async_ready) {  // second arena slot and the ordering events, once
+      const size_t arena = (size_t)h->L * h->Bmax * h->Hkv * h->S * h->dh * h->esz;
+      h->arena_k[1] = dalloc(h, arena);
+      h->arena_v[1] = dalloc(h, arena);
+      h->len_slot[1] = static_cast<int*>(dalloc(h, (size_t)h->Bmax * 4));
+      FV_HIP(hipMemset(h->arena_k[1], 0, arena));
+      FV_HIP(hipMemset(h->arena_v[1], 0, arena));
+      for (int i = 0; i < 2; ++i) {
+        FV_HIP(hipEventCreateWithFlags(&h->ev_ready[i], hipEventDisableTiming));
+        FV_HIP(hipEventCreateWithFlags(&h->ev_done[i], hipEventDisableTiming));
+        FV_HIP(hipEventCreateWithFlags(&h->ev_len[i], hipEventDisableTiming));
+        FV_HIP(hipHostMalloc(reinterpret_cast<void**>(&h->pinned_len[i]), (size_t)h->Bmax * 4,
+                             hipHostMallocDefault));
+      }
+      h->async_ready = true;
+    }
+    hipStream_t cs = static_cast<hipStream_t>(copy_stream);
+    const int sl = h->staged_slot >= 0 ? h->staged_slot : 1 - h->cur_slot;
+    // the slot's previous readers and the previous copy from its length
+    // buffer must be done before it is overwritten
+    if (h->done_recorded[sl]) FV_HIP(hipStreamWaitEvent(cs, h->ev_done[sl], 0));
+    if (h->staged_slot >= 0) FV_HIP(hipStreamWaitEvent(cs, h->ev_ready[sl], 0));
+    if (h->len_recorded[sl]) FV_HIP(hipEventSynchronize(h->ev_len[sl]));
+    std::memcpy(h->pinned_len[sl], len_host, (size_t)batch * 4);
+    (void)hipGetLastError();
+    FV_HIP(hipMemcpyAsync(h->len_slot[sl], h->pinned_len[sl], (size_t)batch * 4,
+                          hipMemcpyHostToDevice, cs));
+    FV_HIP(hipEventRecord(h->ev_len[sl], cs));
+    h->len_recorded[sl] = true;
+    if (ld > 0 && maxlen > 0) {
+      if (h->bf16)
+        launch_prefix_copy<bf16_t>((const bf16_t*)k, (const bf16_t*)v, h->L, batch, batch, ld,
+                                   h->Hkv, h->dh, (bf16_t*)h->arena_k[sl],
+                                   (bf16_t*)h->arena_v[sl], h->Bmax, h->S, h->len_slot[sl], cs);
+      else
+        launch_prefix_copy<float>((const float*)k, (const float*)v, h->L, batch, batch, ld, h->Hkv,
+                                  h->dh, (float*)h->arena_k[sl], (float*)h->arena_v[sl], h->Bmax,
+                                  h->S, h->len_slot[sl], cs);
+      check_launch();
+    }
+    FV_HIP(hipEventRecord(h->ev_ready[sl], cs));
+    h->len_host_slot[sl].assign(len_host, len_host + batch);
+    h->staged_slot = sl;
+    h->staged_batch = batch;
+  });
+}
+
 fv_status fv_decode_step(fv_handle h, float* buffer, const float* t, float* out_chunk,
                          void* stream) {
   if (!h) return FV_ERR_INVALID_ARG;
@@ -657,18 +758,21 @@ fv_status fv_decode_step(fv_handle h, float* buffer, const float* t, float* out_
     check_ptr(buffer, "buffer");
     if (t) check_ptr(t, "t_per_chunk");
     check_ptr(out_chunk, "out_chunk");
+    DeviceScope ds(h->device);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    activate_staged(h, st);
     const float* tt = schedule_or(h, t);
     const float* mod = t ? nullptr : h->mod_cache;
     const int B = h->batch;
     const size_t nbuf = (size_t)B * h->T * h->A * 4, nout = (size_t)B * h->C * h->A * 4;
     if (overlap(buffer, nbuf, out_chunk, nout)) fail(FV_ERR_INVALID_ARG, "buffer and out_chunk overlap");
-    DeviceScope ds(h->device);
-    run_step(h, t ? KIND_STEP : KIND_STEP_CACHED, buffer, tt, out_chunk, nullptr, 0,
-             static_cast<hipStream_t>(stream), [&](hipStream_t s) {
+    run_step(h, t ? KIND_STEP : KIND_STEP_CACHED, buffer, tt, out_chunk, nullptr, 0, st,
+             [&](hipStream_t s) {
                forward(h, buffer, tt, B, h->v, h->L, s, mod);
                launch_euler_shift(buffer, tt, h->v, out_chunk, h->d_noise, h->d_ticket,
                                   h->d_valid, B, h->K, h->C * h->A, s);
              });
+    mark_used(h, st);
   });
 }
 
@@ -680,13 +784,15 @@ fv_status fv_velocity(fv_handle h, const float* buffer, const float* t, float* v
     check_ptr(buffer, "buffer");
     if (t) check_ptr(t, "t");
     check_ptr(v_out, "v_out");
+    DeviceScope ds(h->device);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    activate_staged(h, st);
     const float* tt = schedule_or(h, t);
     const float* mod = t ? nullptr : h->mod_cache;
     const int B = h->batch;
-    DeviceScope ds(h->device);
-    run_step(h, t ? KIND_VELOCITY : KIND_VELOCITY_CACHED, buffer, tt, v_out, nullptr, 0,
-             static_cast<hipStream_t>(stream),
+    run_step(h, t ? KIND_VELOCITY : KIND_VELOCITY_CACHED, buffer, tt, v_out, nullptr, 0, st,
              [&](hipStream_t s) { forward(h, buffer, tt, B, v_out, h->L, s, mod); });
+    mark_used(h, st);
   });
 }
 
@@ -719,6 +825,7 @@ fv_status fv_sequential_decode(fv_handle h, const float* noise, int32_t n_steps,
     check_ptr(out_chunk, "out_chunk");
     if (n_steps < 1 || n_steps > 4096) fail(FV_ERR_INVALID_ARG, "n_steps must be in [1, 4096]");
     DeviceScope ds(h->device);
+    activate_staged(h, static_cast<hipStream_t>(stream));
     float* ts = nullptr;
     for (auto& e : h->tscheds)
       if (e.first == n_steps) ts = e.second;
@@ -740,6 +847,7 @@ fv_status fv_sequential_decode(fv_handle h, const float* noise, int32_t n_steps,
                }
                launch_copy_f32(out_chunk, h->seq_x, n, s);
              });
+    mark_used(h, static_cast<hipStream_t>(stream));
   });
 }
 
@@ -776,6 +884,7 @@ fv_status fv_multibuffer_velocity(fv_handle h, const void* k, const void* v, int
     (void)hipGetLastError();
     // one observation for all N configurations; configuration j (stream j-1)
     // holds j real chunks after N - j padding slots
+    h->staged_slot = -1;  // a pending asynchronous observation is superseded
     h->len_host.assign(N, prefix_len);
     std::vector<int> valid(N);
     for (int j = 0; j < N; ++j) valid[j] = j + 1;
@@ -797,6 +906,7 @@ fv_status fv_multibuffer_velocity(fv_handle h, const void* k, const void* v, int
     h->prefix_set = true;
     run_step(h, KIND_VELOCITY, buffers, t, v_out, nullptr, 0, s,
              [&](hipStream_t st) { forward(h, buffers, t, N, v_out, h->L, st); });
+    mark_used(h, s);
   });
 }
 
@@ -920,12 +1030,14 @@ fv_status fv_debug_forward(fv_handle h, const float* buffer, const float* t, int
     if (n_layers_run < 0 || n_layers_run > h->L) fail(FV_ERR_INVALID_ARG, "n_layers_run out of range");
     DeviceScope ds(h->device);
     hipStream_t s = static_cast<hipStream_t>(stream);
+    activate_staged(h, s);
     (void)hipGetLastError();
     const int B = h->batch;
     forward(h, buffer, t, B, nullptr, n_layers_run, s);
     launch_copy_f32(h_out, h->hres, (size_t)B * h->T * h->W, s);
     if (mod_out) launch_copy_f32(mod_out, h->mod, (size_t)B * h->K * h->Nmod, s);
     check_launch();
+    mark_used(h, s);
   });
 }
 
@@ -946,6 +1058,7 @@ fv_status fv_debug_stage(fv_handle h, int32_t stage, int32_t layer, int32_t reps
         run_stage<float>(h, stage, layer, s);
     }
     check_launch();
+    mark_used(h, s);
   });
 }
 

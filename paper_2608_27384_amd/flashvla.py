@@ -29,7 +29,7 @@ EXPORTED = (
     "fv_sequential_decode", "fv_get_noise_state", "fv_set_noise_state", "fv_set_graph_mode",
     "fv_destroy", "fv_status_string", "fv_last_error", "fv_abi_version", "fv_debug_forward",
     "fv_debug_stage", "fv_query", "fv_set_mask_mode", "fv_set_schedule", "fv_cold_start",
-    "fv_get_valid_slots", "fv_set_valid_slots", "fv_multibuffer_velocity",
+    "fv_get_valid_slots", "fv_set_valid_slots", "fv_multibuffer_velocity", "fv_set_prefix_async",
 )
 
 
@@ -86,6 +86,8 @@ def lib() -> ctypes.CDLL:
             "fv_cold_start": ([H, c_void_p, c_int32, c_int32, c_void_p], S),
             "fv_get_valid_slots": ([H, POINTER(c_int32), c_int32], S),
             "fv_set_valid_slots": ([H, POINTER(c_int32), c_int32], S),
+            "fv_set_prefix_async": ([H, c_void_p, c_void_p, POINTER(c_int32), c_int32, c_int32,
+                                     c_void_p], S),
             "fv_multibuffer_velocity": ([H, c_void_p, c_void_p, c_int32, c_int32, c_void_p,
                                          c_void_p, c_void_p, c_void_p], S),
         }
@@ -170,6 +172,12 @@ def fv_set_prefix(h, k, v, lengths: Sequence[int], ld: int, stream=None) -> None
     lens = (c_int32 * len(lengths))(*[int(x) for x in lengths])
     _check(h, lib().fv_set_prefix(h, _ptr(k), _ptr(v), lens, len(lengths), ld, _stream(stream)),
            "fv_set_prefix")
+
+
+def fv_set_prefix_async(h, k, v, lengths: Sequence[int], ld: int, copy_stream) -> None:
+    lens = (c_int32 * len(lengths))(*[int(x) for x in lengths])
+    _check(h, lib().fv_set_prefix_async(h, _ptr(k), _ptr(v), lens, len(lengths), ld,
+                                        _stream(copy_stream)), "fv_set_prefix_async")
 
 
 def fv_decode_step(h, buffer, t, out_chunk, stream=None) -> None:
@@ -273,6 +281,9 @@ class Expert:
     def set_prefix(self, k, v, lengths, stream=None):
         fv_set_prefix(self.handle, k, v, lengths, k.shape[2], stream)
         self.batch = len(lengths)
+
+    def set_prefix_async(self, k, v, lengths, copy_stream):
+        fv_set_prefix_async(self.handle, k, v, lengths, k.shape[2], copy_stream)
 
     def decode_step(self, buffer, t, out_chunk, stream=None):
         fv_decode_step(self.handle, buffer, t, out_chunk, stream)

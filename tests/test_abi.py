@@ -51,6 +51,7 @@ def test_null_handle_and_null_arguments_are_rejected():
     assert L.fv_cold_start(None, None, 0, 1, None) == fvb.FV_ERR_INVALID_ARG
     assert L.fv_get_valid_slots(None, None, 1) == fvb.FV_ERR_INVALID_ARG
     assert L.fv_set_valid_slots(None, None, 1) == fvb.FV_ERR_INVALID_ARG
+    assert L.fv_set_prefix_async(None, None, None, None, 1, 0, None) == fvb.FV_ERR_INVALID_ARG
     assert L.fv_multibuffer_velocity(None, None, None, 0, 0, None, None, None,
                                      None) == fvb.FV_ERR_INVALID_ARG
     out = ctypes.c_void_p()
