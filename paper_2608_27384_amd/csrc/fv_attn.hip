@@ -331,7 +331,9 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
   constexpr int KT = 32;                 // keys per tile
   constexpr int NT = 64 * NWV;           // threads
   constexpr int RB = 32 * NWV;           // query rows per block
-  constexpr int LDK = DH + 8, LDV = KT + 8;
+  // row pitches: K rows of DH + 8 and V^T rows of KT + 4 elements keep the
+  // 16-byte K and 8-byte V^T fragment reads free of bank conflicts
+  constexpr int LDK = DH + 8, LDV = KT + 4;
   constexpr int NKS = DH / 16;           // 16-wide k steps of Q K^T
   constexpr int NDT = DH / 32;           // 32-row tiles of O^T
   constexpr int VK = KT * DH / 8, VV = DH * KT / 8;  // 16-byte vectors per tile
@@ -419,7 +421,9 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
       const int vi = tid + NT * i;
       if (VV % NT == 0 || vi < VV) {
         const int r = vi / (KT / 8), c = vi - r * (KT / 8);
-        *reinterpret_cast<u32x4*>(&sV[r * LDV + c * 8]) = rv[i];
+        u32x2* dst = reinterpret_cast<u32x2*>(&sV[r * LDV + c * 8]);  // 8-byte aligned rows
+        dst[0] = u32x2{rv[i][0], rv[i][1]};
+        dst[1] = u32x2{rv[i][2], rv[i][3]};
       }
     }
   };
@@ -459,17 +463,21 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
         s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf0, qf[ks], s0, 0, 0, 0);
         s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf1, qf[ks + 1], s1, 0, 0, 0);
       }
-      f32x16 s = s0 + s1;
-      float mt = -INFINITY;
+      f32x16 s = s0 + s1;  // raw scores; the log2-domain scale sl2 > 0 is applied below
+      // keys outside the row's ranges -> -inf, only on tiles that straddle a
+      // range boundary for some row of the wave
+      const bool inside = key0 + KT <= P || (key0 >= klo && key0 + KT <= khi);
+      if (!__all(inside)) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = key0 + 8 * (r >> 2) + 4 * lg + (r & 3);
-        const bool vis = key < P || (key >= klo && key < khi);
-        const float x = vis ? s[r] * sl2 : -INFINITY;
-        s[r] = x;
-        mt = fmaxf(mt, x);
+        for (int r = 0; r < 16; ++r) {
+          const int key = key0 + 8 * (r >> 2) + 4 * lg + (r & 3);
+          if (!(key < P || (key >= klo && key < khi))) s[r] = -INFINITY;
+        }
       }
-      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      float mt = s[0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mt = fmaxf(mt, s[r]);
+      mt = fmaxf(mt, __shfl_xor(mt, 32)) * sl2;
       if (__any(mt > m_run + kHeadroom)) {
         m_pending = mt;
         staged = true;
@@ -479,7 +487,7 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
       float ls = 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(s[r] - m_use);
+        const float p = exp2f(fmaf(s[r], sl2, -m_use));
         s[r] = p;
         ls += p;
       }
