@@ -478,6 +478,9 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
 #pragma unroll
       for (int r = 1; r < 16; ++r) mt = fmaxf(mt, s[r]);
       mt = fmaxf(mt, __shfl_xor(mt, 32)) * sl2;
+      // a row without a reference yet (accumulators and sum still zero)
+      // simply adopts this tile's maximum
+      if (m_run == -INFINITY) m_run = mt;
       if (__any(mt > m_run + kHeadroom)) {
         m_pending = mt;
         staged = true;
