@@ -37,7 +37,8 @@ __global__ void time_embed_kernel(const float* __restrict__ t, T* __restrict__ e
 // h[row] = x[row] w_in + b_in (fp32), then u[row] = rmsnorm(h) (1 + scale) +
 // shift with norm 0's modulation of the row's chunk.  A block takes
 // kEmbRows rows; thread t owns 4 consecutive columns (per 1024-column chunk)
-// of every row, reads w_in once for all rows and keeps the x rows in LDS.
+// of every row, reads w_in once for all rows in batches of independent
+// loads and keeps the x rows in LDS.
 constexpr int kEmbRows = 8;
 
 __device__ __forceinline__ float block_sum_256(float v, float* red) {
@@ -48,42 +49,72 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
-template <typename T>
+template <typename T, int NC>
 __global__ __launch_bounds__(256) void embed_adarms_kernel(
     const float* __restrict__ x, const float* __restrict__ w_in, const float* __restrict__ b_in,
     float* __restrict__ h, const float* __restrict__ mod, int mod_ld, int chunk_len, float eps,
     T* __restrict__ u, int rows, int A, int W) {
-  __shared__ float sx[kEmbRows][64];
+  // thread t owns columns 4t + 1024 i (i < NC, W <= 1024 NC) of kEmbRows
+  // rows; the modulation and the first weight batch are requested before
+  // anything waits, and h stays in registers between the embedding and the
+  // norm
+  constexpr int AB = 16;  // weight rows per batch
+  __shared__ float sx[64][kEmbRows];  // x transposed: one action entry of every row is contiguous
   __shared__ float sred[kEmbRows][4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int row0 = blockIdx.x * kEmbRows;
-  for (int idx = tid; idx < kEmbRows * A; idx += 256) {
-    const int r = idx / A, a = idx - r * A;
-    sx[r][a] = row0 + r < rows ? x[(size_t)(row0 + r) * A + a] : 0.f;
-  }
-  __syncthreads();
-  float ss[kEmbRows];
+  const f32x4 zero4 = f32x4{0.f, 0.f, 0.f, 0.f};
+  f32x4 sv[NC][kEmbRows], bv[NC][kEmbRows], acc[NC][kEmbRows];
 #pragma unroll
-  for (int r = 0; r < kEmbRows; ++r) ss[r] = 0.f;
-  for (int c = 4 * tid; c < W; c += 1024) {
-    f32x4 acc[kEmbRows];
-    const f32x4 bias = *reinterpret_cast<const f32x4*>(b_in + c);
-#pragma unroll
-    for (int r = 0; r < kEmbRows; ++r) acc[r] = bias;
-#pragma unroll 8
-    for (int a = 0; a < A; ++a) {
-      const f32x4 wv = *reinterpret_cast<const f32x4*>(w_in + (size_t)a * W + c);
-#pragma unroll
-      for (int r = 0; r < kEmbRows; ++r) {
-        const float xv = sx[r][a];
-        acc[r] += xv * wv;
-      }
-    }
+  for (int i = 0; i < NC; ++i) {
+    const int c = 4 * tid + 1024 * i;
+    const bool ok = c < W;
+    const f32x4 bias = ok ? *reinterpret_cast<const f32x4*>(b_in + c) : zero4;
 #pragma unroll
     for (int r = 0; r < kEmbRows; ++r) {
-      if (row0 + r < rows) *reinterpret_cast<f32x4*>(h + (size_t)(row0 + r) * W + c) = acc[r];
-      ss[r] += acc[r][0] * acc[r][0] + acc[r][1] * acc[r][1] + acc[r][2] * acc[r][2] +
-               acc[r][3] * acc[r][3];
+      const int row = min(row0 + r, rows - 1);
+      const float* sc = mod + (size_t)(row / chunk_len) * mod_ld;
+      sv[i][r] = ok ? *reinterpret_cast<const f32x4*>(sc + c) : zero4;
+      bv[i][r] = ok ? *reinterpret_cast<const f32x4*>(sc + W + c) : zero4;
+      acc[i][r] = bias;
+    }
+  }
+  for (int idx = tid; idx < kEmbRows * A; idx += 256) {
+    const int r = idx / A, a = idx - r * A;
+    sx[a][r] = row0 + r < rows ? x[(size_t)(row0 + r) * A + a] : 0.f;
+  }
+  __syncthreads();
+  for (int a0 = 0; a0 < A; a0 += AB) {
+    f32x4 wv[NC][AB];
+#pragma unroll
+    for (int i = 0; i < NC; ++i)
+#pragma unroll
+      for (int j = 0; j < AB; ++j) {
+        const int c = 4 * tid + 1024 * i;
+        wv[i][j] = (c < W && a0 + j < A) ? *reinterpret_cast<const f32x4*>(w_in + (size_t)(a0 + j) * W + c)
+                                         : zero4;
+      }
+#pragma unroll
+    for (int j = 0; j < AB; ++j)
+#pragma unroll
+      for (int r = 0; r < kEmbRows; ++r) {
+        const float xv = a0 + j < A ? sx[a0 + j][r] : 0.f;
+#pragma unroll
+        for (int i = 0; i < NC; ++i) acc[i][r] += xv * wv[i][j];
+      }
+  }
+  float ss[kEmbRows];
+#pragma unroll
+  for (int r = 0; r < kEmbRows; ++r) {
+    ss[r] = 0.f;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int c = 4 * tid + 1024 * i;
+      if (c < W) {
+        if (row0 + r < rows) *reinterpret_cast<f32x4*>(h + (size_t)(row0 + r) * W + c) = acc[i][r];
+        ss[r] += acc[i][r][0] * acc[i][r][0] + acc[i][r][1] * acc[i][r][1] +
+                 acc[i][r][2] * acc[i][r][2] + acc[i][r][3] * acc[i][r][3];
+      }
     }
   }
 #pragma unroll
@@ -92,20 +123,21 @@ __global__ __launch_bounds__(256) void embed_adarms_kernel(
     if (lane == 0) sred[r][wave] = v;
   }
   __syncthreads();
-  for (int c = 4 * tid; c < W; c += 1024) {
 #pragma unroll
-    for (int r = 0; r < kEmbRows; ++r) {
-      const int row = row0 + r;
-      if (row >= rows) break;
-      const float tot = sred[r][0] + sred[r][1] + sred[r][2] + sred[r][3];
-      const float rinv = 1.0f / sqrtf(tot / (float)W + eps);
-      const f32x4 hv = *reinterpret_cast<const f32x4*>(h + (size_t)row * W + c);
-      const float* sc = mod + (size_t)(row / chunk_len) * mod_ld;
-      const f32x4 sv = *reinterpret_cast<const f32x4*>(sc + c);
-      const f32x4 bv = *reinterpret_cast<const f32x4*>(sc + W + c);
-      store4<T>(u + (size_t)row * W + c, hv[0] * rinv * (1.0f + sv[0]) + bv[0],
-                hv[1] * rinv * (1.0f + sv[1]) + bv[1], hv[2] * rinv * (1.0f + sv[2]) + bv[2],
-                hv[3] * rinv * (1.0f + sv[3]) + bv[3]);
+  for (int r = 0; r < kEmbRows; ++r) {
+    const int row = row0 + r;
+    if (row >= rows) break;
+    const float tot = sred[r][0] + sred[r][1] + sred[r][2] + sred[r][3];
+    const float rinv = 1.0f / sqrtf(tot / (float)W + eps);
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int c = 4 * tid + 1024 * i;
+      if (c >= W) continue;
+      const f32x4 hv = acc[i][r];
+      store4<T>(u + (size_t)row * W + c, hv[0] * rinv * (1.0f + sv[i][r][0]) + bv[i][r][0],
+                hv[1] * rinv * (1.0f + sv[i][r][1]) + bv[i][r][1],
+                hv[2] * rinv * (1.0f + sv[i][r][2]) + bv[i][r][2],
+                hv[3] * rinv * (1.0f + sv[i][r][3]) + bv[i][r][3]);
     }
   }
 }
@@ -213,10 +245,10 @@ __global__ __launch_bounds__(256) void adarms_kernel(const float* __restrict__ h
 // ------------------------------------- final FiLM RMSNorm + velocity head
 // v[row] = (rmsnorm(h) (1 + scale) + shift) w_out + b_out, fp32.  A block
 // handles kFinalRows rows: each wave normalises one row into LDS (every load
-// of the row issued before use).  Then each output (row, a) is summed by
-// `parts` threads over interleaved slices of the width, reading w_out in
-// unrolled batches of independent loads, and the slices are added in a
-// fixed order.
+// of the row issued before use).  Then thread (part, a) sums output column a
+// of all the block's rows over one contiguous slice of the width, reading
+// w_out in batches of 32 independent loads that serve every row, and the
+// slices are added in a fixed order.
 constexpr int kFinalRows = 4;
 constexpr int kMaxW = 2048;
 __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ h,
@@ -226,7 +258,7 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ h,
                                                     const float* __restrict__ b_out,
                                                     float* __restrict__ v, int rows, int W,
                                                     int A) {
-  extern __shared__ float smem[];  // su [kFinalRows][W], sp [256]
+  extern __shared__ float smem[];  // su [kFinalRows][W], sp [parts][kFinalRows][A]
   float* su = smem;
   float* sp = su + kFinalRows * W;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, tid = threadIdx.x;
@@ -256,29 +288,37 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ h,
     }
   }
   __syncthreads();
-  const int nout = kFinalRows * A;  // <= 256
-  const int parts = 256 / nout;
-  const int o = tid % nout, part = tid / nout;
-  const int r = o / A, a = o - r * A;
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  // thread (part, a): output column a of all kFinalRows rows over the
+  // width slice `part`; weight loads go out 32 at a time, each used for
+  // every row; the slices are then added in a fixed order
+  constexpr int KB = 32;
+  const int parts = 256 / A;
+  const int part = tid / A, a = tid - part * A;
+  const int kr = (W + parts - 1) / parts;
+  const int k0 = part * kr, k1 = min(W, k0 + kr);
+  float acc[kFinalRows] = {};
   if (part < parts) {
-    const float* ur = su + r * W;
-    int n = part;
-    for (; n + 7 * parts < W; n += 8 * parts) {
-      float wv[8];
+    for (int kb = k0; kb < k1; kb += KB) {
+      float wv[KB];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) wv[u] = w_out[(size_t)(n + u * parts) * A + a];
+      for (int j = 0; j < KB; ++j) wv[j] = kb + j < k1 ? w_out[(size_t)(kb + j) * A + a] : 0.f;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) acc[u] = fmaf(ur[n + u * parts], wv[u], acc[u]);
+      for (int j = 0; j < KB; ++j)
+#pragma unroll
+        for (int r = 0; r < kFinalRows; ++r)
+          acc[r] = fmaf(kb + j < k1 ? su[r * W + kb + j] : 0.f, wv[j], acc[r]);
     }
-    for (; n < W; n += parts) acc[0] = fmaf(ur[n], w_out[(size_t)n * A + a], acc[0]);
+#pragma unroll
+    for (int r = 0; r < kFinalRows; ++r) sp[(part * kFinalRows + r) * A + a] = acc[r];
   }
-  sp[tid] = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
   __syncthreads();
-  if (tid < nout && row0 + r < rows) {
-    float tot = b_out[a];
-    for (int p = 0; p < parts; ++p) tot += sp[p * nout + tid];
-    v[(size_t)(row0 + r) * A + a] = tot;
+  if (tid < kFinalRows * A) {
+    const int r = tid / A, aa = tid - r * A;
+    if (row0 + r < rows) {
+      float tot = b_out[aa];
+      for (int p = 0; p < parts; ++p) tot += sp[(p * kFinalRows + r) * A + aa];
+      v[(size_t)(row0 + r) * A + aa] = tot;
+    }
   }
 }
 
@@ -495,8 +535,13 @@ template <typename T>
 void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, float* h,
                          const float* mod, int mod_ld, int chunk_len, float eps, T* u, int rows,
                          int A, int W, hipStream_t s) {
-  hipLaunchKernelGGL((embed_adarms_kernel<T>), dim3((rows + kEmbRows - 1) / kEmbRows), dim3(256),
-                     0, s, x, w_in, b_in, h, mod, mod_ld, chunk_len, eps, u, rows, A, W);
+  const dim3 grid((rows + kEmbRows - 1) / kEmbRows);
+  if (W <= 1024)
+    hipLaunchKernelGGL((embed_adarms_kernel<T, 1>), grid, dim3(256), 0, s, x, w_in, b_in, h, mod,
+                       mod_ld, chunk_len, eps, u, rows, A, W);
+  else
+    hipLaunchKernelGGL((embed_adarms_kernel<T, 2>), grid, dim3(256), 0, s, x, w_in, b_in, h, mod,
+                       mod_ld, chunk_len, eps, u, rows, A, W);
 }
 
 template <typename T>
@@ -522,7 +567,7 @@ void launch_adarms(const float* h, const float* mod, int mod_ld, int scale_off, 
 void launch_final(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
                   float eps, const float* w_out, const float* b_out, float* v, int rows, int W,
                   int A, hipStream_t s) {
-  const size_t lds = (size_t)(kFinalRows * W + 256) * sizeof(float);
+  const size_t lds = (size_t)(kFinalRows * W + 256 * kFinalRows) * sizeof(float);
   hipLaunchKernelGGL(final_kernel, dim3((rows + kFinalRows - 1) / kFinalRows), dim3(256), lds, s, h, mod, mod_ld,
                      scale_off, chunk_len, eps, w_out, b_out, v, rows, W, A);
 }
