@@ -47,8 +47,25 @@ def build(jobs: int = 4) -> str:
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stdout + r.stderr)
+    _check_kernel_stubs(tmp)
     os.replace(tmp, OUT)
     return OUT
+
+
+def _check_kernel_stubs(lib: str) -> None:
+    """Fails if a kernel launched from host code has no host-side stub.
+
+    A kernel template whose instantiation fails in one of the two compiler
+    passes can be dropped without a diagnostic; the library then links but
+    the launch cannot work.  nm lists such kernels as undefined stubs."""
+    r = subprocess.run(["nm", "-C", "--undefined-only", lib], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("nm failed on " + lib + ":\n" + r.stderr)
+    missing = [ln.strip() for ln in r.stdout.splitlines() if "__device_stub__" in ln]
+    if missing:
+        os.remove(lib)
+        raise RuntimeError("kernels without a host stub (instantiation failed):\n" +
+                           "\n".join(missing))
 
 
 if __name__ == "__main__":

@@ -4,14 +4,17 @@
 // projection, packed gate/up, down projection) is C = A * W with A the
 // activations [M][K] (row-major) and W stored output-major as Bt [N][K].
 //
-// Block: NW waves (4 or 8).  Tile BM x BN; k is staged through LDS 128 bytes
-// per row (64 bf16 / 32 fp32) at a time in two buffers.  While a wave
+// Block: NW waves (2, 4 or 8).  Tile BM x BN; k is staged through LDS 128
+// bytes per row (64 bf16 / 32 fp32) at a time in two buffers.  While a wave
 // multiplies the tile in one buffer with 32x32 MFMA instructions, the
 // registers holding the next tile are written to the other buffer piece by
 // piece between k-steps, and every freed register piece immediately issues
-// its global load of the tile after that, so MFMA work, LDS writes and global
-// loads overlap; one barrier per k-tile.  Rows of A beyond M re-read row M-1
-// (never stored).
+// its global load of the tile after that; the MFMA operands of the next
+// k-step are read from LDS while the current k-step's MFMAs run, and the
+// instruction order interleaves MFMAs with those reads, stores and loads.
+// One barrier per k-tile.  Rows of A beyond M re-read row M-1 (never
+// stored).  Large grids walk their tiles in an order that keeps the blocks
+// each of the chip's 8 dies runs together on shared operands.
 //
 // Split-K (KS > 1): block z of a tile accumulates k-tiles [z*nk/KS,
 // (z+1)*nk/KS) and writes its fp32 partial tile to a workspace; a second,
@@ -63,6 +66,31 @@ __device__ __forceinline__ int acc_row(int r, int lane) {
   return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
 }
 
+// Output tile of this block.  Block b of a launch runs on XCD b % 8 (the
+// chip's 8 dies, each with its own L2).  When the grid is large enough, the
+// (x, y) block index is remapped so that each die takes a contiguous range
+// of tiles, walked in groups kTileGroup row panels tall, column by column:
+// the tiles a die runs together then share A row panels and weight column
+// blocks in its L2 instead of fetching them from memory once per die.
+constexpr int kTileGroup = 8;
+__device__ __forceinline__ void tile_of(int& tm, int& tn) {
+  const int nN = gridDim.x, nM = gridDim.y, nb = nN * nM;
+  if (nb < 64) {
+    tm = blockIdx.y;
+    tn = blockIdx.x;
+    return;
+  }
+  const int b = blockIdx.y * nN + blockIdx.x;
+  const int per = nb >> 3, rem = nb & 7;  // dies x < rem take per + 1 tiles
+  const int x = b & 7, s = b >> 3;
+  const int L = x * per + min(x, rem) + s;
+  const int gsz = kTileGroup * nN;
+  const int g = L / gsz, i = L - g * gsz;
+  const int gm = min(kTileGroup, nM - g * kTileGroup);
+  tm = g * kTileGroup + i % gm;
+  tn = i / gm;
+}
+
 template <typename T, int BM, int BN, int NW, int WGM, class Epi>
 __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ A,
                                                        const T* __restrict__ Bt, int M, int N,
@@ -76,18 +104,19 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ A,
   constexpr int EPV = 16 / (int)sizeof(T);  // elements per 16-byte vector
   constexpr int BK = 8 * EPV;               // 128 bytes of k per row and stage
   constexpr int LDR = BK + EPV;             // LDS row pitch (one vector of padding)
-  constexpr int VA = BM * 8, VB = BN * 8;   // 16-byte vectors per stage
-  constexpr int NA = (VA + NT - 1) / NT, NB = (VB + NT - 1) / NT;
+  constexpr int NA = BM * 8 / NT, NB = BN * 8 / NT, NP = NA + NB;  // 16-byte pieces per thread
   constexpr int NSTEP = BK / MF::KM;
   static_assert(FM >= 1 && FN >= 1 && WGM * WGN == NW, "bad tile");
+  static_assert((BM * 8) % NT == 0 && (BN * 8) % NT == 0 && NSTEP % 2 == 0, "bad tile");
 
-  __shared__ __attribute__((aligned(16))) T sA[2][BM * LDR];
-  __shared__ __attribute__((aligned(16))) T sB[2][BN * LDR];
+  __shared__ __attribute__((aligned(16))) T sm[2 * (BM + BN) * LDR];  // [buf][A rows ; B rows]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WGM, wn = wave / WGM;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int arow = wm * WTM, brow = wn * WTN;
+  int tm, tn;
+  tile_of(tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int arow = wm * WTM, brow = BM + wn * WTN;  // fragment rows in the stage
   const int nk_all = K / BK;
   const int kz = blockIdx.z;
   const int kt0 = (kz * nk_all) / KS, kt1 = ((kz + 1) * nk_all) / KS;
@@ -99,93 +128,95 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ A,
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
 
-  u32x4 ra[NA], rb[NB];
+  // Thread piece p: 16 bytes of row r, k-vector c of a stage (A rows first).
+  const T* gp[NP];
+  int lp[NP];
 #pragma unroll
-  for (int i = 0; i < NA; ++i) ra[i] = u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-  for (int i = 0; i < NB; ++i) rb[i] = u32x4{0u, 0u, 0u, 0u};
+  for (int p = 0; p < NP; ++p) {
+    const bool isa = p < NA;
+    const int vi = tid + NT * (isa ? p : p - NA);
+    const int r = vi >> 3, c = vi & 7;
+    gp[p] = isa ? A + (size_t)min(m0 + r, M - 1) * K + c * EPV
+                : Bt + (size_t)(n0 + r) * K + c * EPV;
+    lp[p] = (isa ? r : BM + r) * LDR + c * EPV;
+  }
 
-  // Prologue: tile kt0 into LDS[0], tile kt0+1 into registers.
+  // Prologue: stage kt0 into LDS buffer 0, stage kt0+1 into registers.
+  u32x4 rg[NP];
 #pragma unroll
-  for (int step = 0; step < 2; ++step) {
-    const int k0 = step == 0 ? kt0 * BK : min((kt0 + 1) * BK, klast);
+  for (int p = 0; p < NP; ++p) rg[p] = *reinterpret_cast<const u32x4*>(gp[p] + kt0 * BK);
 #pragma unroll
-    for (int i = 0; i < NA; ++i) {
-      const int vi = tid + NT * i;
-      if (VA % NT == 0 || vi < VA) {
-        const int r = vi >> 3, c = vi & 7;
-        const int gr = min(m0 + r, M - 1);
-        ra[i] = *reinterpret_cast<const u32x4*>(A + (size_t)gr * K + k0 + c * EPV);
-      }
-    }
+  for (int p = 0; p < NP; ++p) *reinterpret_cast<u32x4*>(&sm[lp[p]]) = rg[p];
+  {
+    const int k1 = min((kt0 + 1) * BK, klast);
 #pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      const int vi = tid + NT * i;
-      if (VB % NT == 0 || vi < VB) {
-        const int r = vi >> 3, c = vi & 7;
-        rb[i] = *reinterpret_cast<const u32x4*>(Bt + (size_t)(n0 + r) * K + k0 + c * EPV);
-      }
-    }
-    if (step == 0) {
-#pragma unroll
-      for (int i = 0; i < NA; ++i) {
-        const int vi = tid + NT * i;
-        if (VA % NT == 0 || vi < VA)
-          *reinterpret_cast<u32x4*>(&sA[0][(vi >> 3) * LDR + (vi & 7) * EPV]) = ra[i];
-      }
-#pragma unroll
-      for (int i = 0; i < NB; ++i) {
-        const int vi = tid + NT * i;
-        if (VB % NT == 0 || vi < VB)
-          *reinterpret_cast<u32x4*>(&sB[0][(vi >> 3) * LDR + (vi & 7) * EPV]) = rb[i];
-      }
-    }
+    for (int p = 0; p < NP; ++p) rg[p] = *reinterpret_cast<const u32x4*>(gp[p] + k1);
   }
   __syncthreads();
 
+  // Fragments are double-buffered: those of k-step ks+1 are read while the
+  // MFMAs of k-step ks run.  The next stage's register pieces go to the
+  // other LDS buffer during k-steps 0..NSTEP-2 (each freed register then
+  // loads its piece of the stage after that); one barrier, placed before the
+  // last k-step, publishes the new stage, whose first fragments are read
+  // while the last k-step's MFMAs run.
   const int lr = lane & 31, lk = MF::KG * (lane >> 5);
+  typename MF::frag af[2][FM], bfr[2][FN];
+  auto read_frags = [&](int slot, int buf, int ks) __attribute__((always_inline)) {
+    const T* base = sm + buf * (BM + BN) * LDR + ks * MF::KM + lk;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) af[slot][i] = MF::load(base + (arow + 32 * i + lr) * LDR);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) bfr[slot][j] = MF::load(base + (brow + 32 * j + lr) * LDR);
+  };
+  read_frags(0, 0, 0);
   for (int kt = kt0; kt < kt1; ++kt) {
     const int cur = (kt - kt0) & 1;
     const int knext = min((kt + 2) * BK, klast);  // unconditional prefetch (clamped)
+    T* const nxt = sm + (cur ^ 1) * (BM + BN) * LDR;
 #pragma unroll
     for (int ks = 0; ks < NSTEP; ++ks) {
-      typename MF::frag af[FM], bfr[FN];
+      const int cb = ks & 1;
+      if (ks + 1 < NSTEP) {
+        read_frags(cb ^ 1, cur, ks + 1);
+      } else {
+        __syncthreads();
+        read_frags(cb ^ 1, cur ^ 1, 0);
+      }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
-        af[i] = MF::load(&sA[cur][(arow + 32 * i + lr) * LDR + ks * MF::KM + lk]);
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
-        bfr[j] = MF::load(&sB[cur][(brow + 32 * j + lr) * LDR + ks * MF::KM + lk]);
+        for (int j = 0; j < FN; ++j) acc[i][j] = MF::mma(af[cb][i], bfr[cb][j], acc[i][j]);
+      int nw = 0;
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+      for (int p = 0; p < NP; ++p) {
+        if (ks + 1 == NSTEP || (p * (NSTEP - 1)) / NP != ks) continue;
+        *reinterpret_cast<u32x4*>(&nxt[lp[p]]) = rg[p];
+        rg[p] = *reinterpret_cast<const u32x4*>(gp[p] + knext);
+        ++nw;
+      }
+      // issue order: one fragment read after each MFMA, then one LDS store
+      // and one global load per MFMA, then the remaining MFMAs
+      constexpr int nrd = FM + FN < FM * FN ? FM + FN : FM * FN;
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = MF::mma(af[i], bfr[j], acc[i][j]);
-      // register pieces of the next tile assigned to this k-step: store them
-      // into the other buffer, then reload them with the tile after that
+      for (int q = 0; q < nrd; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
 #pragma unroll
-      for (int i = 0; i < NA; ++i) {
-        if ((i * NSTEP) / NA != ks) continue;
-        const int vi = tid + NT * i;
-        if (VA % NT == 0 || vi < VA) {
-          const int r = vi >> 3, c = vi & 7;
-          *reinterpret_cast<u32x4*>(&sA[cur ^ 1][r * LDR + c * EPV]) = ra[i];
-          const int gr = min(m0 + r, M - 1);
-          ra[i] = *reinterpret_cast<const u32x4*>(A + (size_t)gr * K + knext + c * EPV);
+      for (int q = 0; q < NP; ++q) {
+        if (q < nw && nrd + q < FM * FN) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
         }
       }
 #pragma unroll
-      for (int i = 0; i < NB; ++i) {
-        if ((i * NSTEP) / NB != ks) continue;
-        const int vi = tid + NT * i;
-        if (VB % NT == 0 || vi < VB) {
-          const int r = vi >> 3, c = vi & 7;
-          *reinterpret_cast<u32x4*>(&sB[cur ^ 1][r * LDR + c * EPV]) = rb[i];
-          rb[i] = *reinterpret_cast<const u32x4*>(Bt + (size_t)(n0 + r) * K + knext + c * EPV);
-        }
-      }
+      for (int q = 0; q < FM * FN; ++q)
+        if (q >= nrd + nw) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     }
-    __syncthreads();
   }
+  const int ar = wm * WTM, bc = wn * WTN;
 
   if (KS > 1) {
     // Partial tile -> workspace, row-major [KS][M][N] fp32 (lanes of a row
@@ -195,16 +226,16 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ A,
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
-        const int col = n0 + brow + 32 * j + (lane & 31);
+        const int col = n0 + bc + 32 * j + (lane & 31);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int row = m0 + arow + 32 * i + acc_row(r, lane);
+          const int row = m0 + ar + 32 * i + acc_row(r, lane);
           if (row < M) part[(size_t)row * N + col] = acc[i][j][r];
         }
       }
     return;
   }
-  epi.template apply<FM, FN>(acc, m0 + arow, n0 + brow, lane, M);
+  epi.template apply<FM, FN>(acc, m0 + ar, n0 + bc, lane, M);
 }
 
 // Sum of the KS split partials of each tile, in split order, followed by the
