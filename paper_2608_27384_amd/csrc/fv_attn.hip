@@ -11,10 +11,10 @@
 // probability exactly 0; tiles outside every row's ranges are not visited.
 //
 // Work split: the query rows of one (stream, kv head) are the (token, head)
-// pairs of its query-head group, flattened token-major; a block of 4 waves
-// takes 64 consecutive rows (16 per wave; RG groups of 16 rows per wave share
-// every K and V fragment read from LDS), so rows of all heads that share the
-// kv head reuse one K/V tile.  The next K/V tile is loaded into registers
+// pairs of its query-head group, flattened token-major; a block takes
+// consecutive rows, 16 per wave (bf16: 8 waves, 128 rows; fp32: 4 waves, 64
+// rows, RG groups of 16 rows per wave sharing every K and V fragment read
+// from LDS), so rows of all heads that share the kv head reuse one K/V tile.  The next K/V tile is loaded into registers
 // while the current one is multiplied.  Rows of a block may straddle a chunk
 // boundary; each lane masks with its own row's limit.  Optionally the key
 // tiles of a block are split over gridDim.z blocks whose normalised partial
@@ -36,11 +36,11 @@ constexpr float kSlack = 8.0f;  // lazy softmax reference slack (log2 units)
 constexpr float kHeadroom = 64.0f;  // fixed-reference headroom of the bf16 kernel (log2 units)
 constexpr int kRG = 1;          // 16-row MFMA groups per wave
 constexpr int kRowsPerBlock = 4 * 16 * kRG;
-constexpr int kAttn32Waves = 4;  // bf16 kernel: 4 waves x 32 rows
+constexpr int kAttn16Waves = 8;  // bf16 kernel: 8 waves x 16 rows
 
 template <typename T>
 constexpr int rows_per_block() {
-  return sizeof(T) == 2 ? 32 * kAttn32Waves : kRowsPerBlock;
+  return sizeof(T) == 2 ? 16 * kAttn16Waves : kRowsPerBlock;
 }
 
 // Key tiles a block visits: the prefix tiles [0, nA), then the tiles of the
@@ -318,29 +318,30 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
 }
 
-// bf16 path with 32x32x16 MFMAs.  A wave owns 32 query rows; S^T = K Q^T
-// gives a lane the scores of query (lane % 32) for 16 keys of a 32-key tile,
-// and those scores, rounded to bf16, are directly the B operand of
-// O^T += V^T P^T once the V^T fragment reads the same key order (lane group
-// g = lane / 32 holds keys {4g..4g+3, 8+4g..8+4g+3} of each 16-key half).
-// Per 16 k of the reduction a 32x32x16 MFMA reads 1 KB of operands for
-// 32K flops, half the LDS traffic per flop of the 16x16x32 form.
+// bf16 path with 16x16x32 MFMAs and 16 query rows per wave: 8 waves share
+// each K/V tile of a 128-row block.  A wave's state (O^T 256 x 16 in 64
+// registers, Q^T fragments in 32) lets two waves share a SIMD, so one
+// wave's softmax arithmetic and fixed costs overlap the other's MFMAs (a
+// 32-row wave needs 128 + 64 registers for the same and runs alone).  S^T = K Q^T per 16-key half h gives lane l
+// the scores of query l % 16 for keys 16 h + 4 g + 0..3 (g = l / 16); the 8
+// scores of both halves, rounded to bf16, are the B operand of
+// O^T += V^T P^T with the MFMA's k index 8 g + e standing for key
+// 4 g + e (e < 4) or 16 + 4 g + e - 4 (e >= 4), and the V^T fragment reads
+// the same two 4-key runs.
 template <int DH, int NWV>
-__global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64 * NWV) void attn16_kernel(AttnArgs a) {
   using T = bf16_t;
   constexpr int KT = 32;                 // keys per tile
   constexpr int NT = 64 * NWV;           // threads
-  constexpr int RB = 32 * NWV;           // query rows per block
-  // row pitches: K rows of DH + 8 and V^T rows of KT + 4 elements keep the
-  // 16-byte K and 8-byte V^T fragment reads free of bank conflicts
+  constexpr int RB = 16 * NWV;           // query rows per block
   constexpr int LDK = DH + 8, LDV = KT + 4;
-  constexpr int NKS = DH / 16;           // 16-wide k steps of Q K^T
-  constexpr int NDT = DH / 32;           // 32-row tiles of O^T
+  constexpr int NKS = DH / 32;           // 32-wide k steps of Q K^T
+  constexpr int NDT = DH / 16;           // 16-row tiles of O^T
   constexpr int VK = KT * DH / 8, VV = DH * KT / 8;  // 16-byte vectors per tile
   constexpr int NVK = (VK + NT - 1) / NT, NVV = (VV + NT - 1) / NT;
   __shared__ __attribute__((aligned(16))) T sK[KT * LDK];
   __shared__ __attribute__((aligned(16))) T sV[DH * LDV];
-  __shared__ __attribute__((aligned(16))) T sO[NWV][32 * LDK];  // output staging
+  __shared__ __attribute__((aligned(16))) T sO[NWV][16 * LDK];  // output staging
 
   const int G = a.n_q_heads / a.n_kv_heads;
   const int rows_bg = a.tokens * G;
@@ -350,11 +351,11 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int P = a.len[b];
   const int C = a.chunk_len;
-  const int l32 = lane & 31, lg = lane >> 5;
+  const int l16 = lane & 15, lg = lane >> 4;
 
   const int K = a.tokens / C;
   const int first = K - a.n_valid[b];
-  const int rq = tile0 + 32 * wave + l32;
+  const int rq = tile0 + 16 * wave + l16;
   const bool valid = rq < rows_bg;
   const int rqc = valid ? rq : rows_bg - 1;
   const int tok = rqc / G;
@@ -367,18 +368,18 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
   const KeyTiles kts = key_tiles(P, C, K, first, a.mask_mode, tile0 / G, rlast / G, KT);
   const int kt_begin = (split * kts.n) / a.n_split, kt_end = ((split + 1) * kts.n) / a.n_split;
 
-  // Q^T fragments (B operand): query l32, dh 16 ks + 8 lg .. + 8
+  // Q^T fragments (B operand): query l16, dh 32 ks + 8 lg .. + 8
   bf16x8 qf[NKS];
   {
     const T* qrow = reinterpret_cast<const T*>(a.q) +
                     ((size_t)(b * a.tokens + tok) * a.n_q_heads + head) * DH;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks)
-      qf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(qrow + 16 * ks + 8 * lg));
+      qf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(qrow + 32 * ks + 8 * lg));
   }
-  f32x16 acc[NDT];
+  f32x4 acc[NDT];
 #pragma unroll
-  for (int dt = 0; dt < NDT; ++dt) acc[dt] = f32x16{};
+  for (int dt = 0; dt < NDT; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
   const T* kbase = reinterpret_cast<const T*>(a.karena) +
@@ -437,8 +438,8 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
   // processed again against the raised reference.
   const int kt_clamp = max(kt_begin, kt_end - 1);
   load_tile(kts.tile(min(kt_begin, kt_clamp)));
-  int kt = kt_begin;    // virtual tile index
-  bool staged = false;  // tile kt already in LDS (after a restart)
+  int kt = kt_begin;
+  bool staged = false;
   float m_pending = -INFINITY;
   while (kt < kt_end) {
     for (; kt < kt_end; ++kt) {
@@ -451,35 +452,37 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
       }
       staged = false;
 
-      // S^T (32 keys x 32 queries); lane: query l32, key 8(r/4) + 4 lg + r%4;
-      // two independent MFMA chains (even / odd k steps) halve the chain latency
-      f32x16 s0 = f32x16{}, s1 = f32x16{};
+      // S^T per 16-key half: two chains each (even / odd k steps)
+      f32x4 s[2][2] = {{f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}},
+                       {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}}};
 #pragma unroll
-      for (int ks = 0; ks < NKS; ks += 2) {
-        const bf16x8 kf0 = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u16x8*>(&sK[l32 * LDK + 16 * ks + 8 * lg]));
-        const bf16x8 kf1 = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u16x8*>(&sK[l32 * LDK + 16 * ks + 16 + 8 * lg]));
-        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf0, qf[ks], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf1, qf[ks + 1], s1, 0, 0, 0);
+      for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const bf16x8 kf = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u16x8*>(&sK[(16 * h + l16) * LDK + 32 * ks + 8 * lg]));
+          s[h][ks & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], s[h][ks & 1], 0, 0, 0);
+        }
+      // sc[e] (e < 4): key 4 lg + e;  sc[4 + e]: key 16 + 4 lg + e
+      float sc[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        sc[e] = s[0][0][e] + s[0][1][e];
+        sc[4 + e] = s[1][0][e] + s[1][1][e];
       }
-      f32x16 s = s0 + s1;  // raw scores; the log2-domain scale sl2 > 0 is applied below
-      // keys outside the row's ranges -> -inf, only on tiles that straddle a
-      // range boundary for some row of the wave
       const bool inside = key0 + KT <= P || (key0 >= klo && key0 + KT <= khi);
       if (!__all(inside)) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = key0 + 8 * (r >> 2) + 4 * lg + (r & 3);
-          if (!(key < P || (key >= klo && key < khi))) s[r] = -INFINITY;
+        for (int e = 0; e < 8; ++e) {
+          const int key = key0 + 16 * (e >> 2) + 4 * lg + (e & 3);
+          if (!(key < P || (key >= klo && key < khi))) sc[e] = -INFINITY;
         }
       }
-      float mt = s[0];
+      float mt = sc[0];
 #pragma unroll
-      for (int r = 1; r < 16; ++r) mt = fmaxf(mt, s[r]);
+      for (int e = 1; e < 8; ++e) mt = fmaxf(mt, sc[e]);
+      mt = fmaxf(mt, __shfl_xor(mt, 16));
       mt = fmaxf(mt, __shfl_xor(mt, 32)) * sl2;
-      // a row without a reference yet (accumulators and sum still zero)
-      // simply adopts this tile's maximum
       if (m_run == -INFINITY) m_run = mt;
       if (__any(mt > m_run + kHeadroom)) {
         m_pending = mt;
@@ -488,34 +491,29 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
       }
       const float m_use = m_run == -INFINITY ? 0.f : m_run;
       float ls = 0.f;
+      u16x8 pb;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(fmaf(s[r], sl2, -m_use));
-        s[r] = p;
+      for (int e = 0; e < 8; ++e) {
+        const float p = exp2f(fmaf(sc[e], sl2, -m_use));
         ls += p;
+        pb[e] = f32_to_bf16(p);
       }
+      ls += __shfl_xor(ls, 16);
       l_run += ls + __shfl_xor(ls, 32);
-      // O^T (dh x queries) += V^T P^T over two 16-key halves
+      const bf16x8 pf = __builtin_bit_cast(bf16x8, pb);
+      // O^T (dh x queries) += V^T P^T: dh row 16 dt + l16, keys 4 lg + 0..3
+      // and 16 + 4 lg + 0..3
 #pragma unroll
-      for (int kc = 0; kc < 2; ++kc) {
-        u16x8 pb;
-#pragma unroll
-        for (int r = 0; r < 8; ++r) pb[r] = f32_to_bf16(s[8 * kc + r]);
-        const bf16x8 pf = __builtin_bit_cast(bf16x8, pb);
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-          const T* vr = &sV[(32 * dt + l32) * LDV + 16 * kc + 4 * lg];
-          const u16x4 lo = *reinterpret_cast<const u16x4*>(vr);
-          const u16x4 hi = *reinterpret_cast<const u16x4*>(vr + 8);
-          const bf16x8 vf = __builtin_bit_cast(
-              bf16x8, u16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
-          acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[dt], 0, 0, 0);
-        }
+      for (int dt = 0; dt < NDT; ++dt) {
+        const T* vr = &sV[(16 * dt + l16) * LDV + 4 * lg];
+        const u16x4 lo = *reinterpret_cast<const u16x4*>(vr);
+        const u16x4 hi = *reinterpret_cast<const u16x4*>(vr + 16);
+        const bf16x8 vf = __builtin_bit_cast(
+            bf16x8, u16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, acc[dt], 0, 0, 0);
       }
     }
     if (staged) {
-      // raise the reference of the rows that need it (a row's new reference
-      // is its tile maximum), rescale their accumulators, then redo tile kt
       const float m_new = m_pending > m_run + kHeadroom ? m_pending : m_run;
       const float alpha = m_run == -INFINITY ? 0.f : exp2f(m_run - m_new);
       l_run *= alpha;
@@ -525,23 +523,19 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
     }
   }
 
-  // Normalised output (a split with no visible key stores 0): the wave's
-  // 32 x DH tile goes to its own LDS rows [query][dh] and then to global
-  // memory as whole rows, 16 contiguous bytes per lane.
+  // Normalised output through LDS: lane (query l16, group lg) holds dh
+  // 16 dt + 4 lg + 0..3; rows then go out whole, 16 bytes per lane.
   const size_t R = (size_t)a.B * a.tokens * a.n_q_heads;
   {
     const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
     T* so = sO[wave];
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
+    for (int dt = 0; dt < NDT; ++dt) {
+      u16x4 w;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        // registers 4q..4q+3 hold dh 32 dt + 8 q + 4 lg + 0..3
-        u16x4 w;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) w[i] = f32_to_bf16(acc[dt][4 * q + i] * inv);
-        *reinterpret_cast<u16x4*>(so + l32 * LDK + 32 * dt + 8 * q + 4 * lg) = w;
-      }
+      for (int i = 0; i < 4; ++i) w[i] = f32_to_bf16(acc[dt][i] * inv);
+      *reinterpret_cast<u16x4*>(so + l16 * LDK + 16 * dt + 4 * lg) = w;
+    }
     if (a.n_split > 1 && lg == 0 && valid) {
       const size_t grow = (size_t)(b * a.tokens + tok) * a.n_q_heads + head;
       a.part_ml[((size_t)split * R + grow) * 2 + 0] = m_run;
@@ -552,9 +546,9 @@ __global__ __launch_bounds__(64 * NWV) void attn32_kernel(AttnArgs a) {
   {
     constexpr int CPR = DH / 8;  // 16-byte chunks per row
     const T* so = sO[wave];
-    for (int idx = lane; idx < 32 * CPR; idx += 64) {
+    for (int idx = lane; idx < 16 * CPR; idx += 64) {
       const int row = idx / CPR, c = idx - row * CPR;
-      const int rq2 = tile0 + 32 * wave + row;
+      const int rq2 = tile0 + 16 * wave + row;
       if (rq2 < rows_bg) {
         const int tok2 = rq2 / G;
         const int head2 = g * G + (rq2 - tok2 * G);
@@ -631,7 +625,7 @@ void launch_dh(const AttnArgs& a, hipStream_t s, int parts) {
   dim3 grid((a.tokens * G + RB - 1) / RB, a.B * a.n_kv_heads, a.n_split);
   if (parts & 1) {
     if constexpr (sizeof(T) == 2)
-      hipLaunchKernelGGL((attn32_kernel<DH, kAttn32Waves>), grid, dim3(64 * kAttn32Waves), 0, s, a);
+      hipLaunchKernelGGL((attn16_kernel<DH, kAttn16Waves>), grid, dim3(64 * kAttn16Waves), 0, s, a);
     else
       hipLaunchKernelGGL((attn_kernel<T, DH, KT, kRG>), grid, dim3(256), 0, s, a);
   }
