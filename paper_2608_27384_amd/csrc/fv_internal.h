@@ -74,10 +74,15 @@ __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float a, float b, floa
   *reinterpret_cast<u16x4*>(p) = u16x4{f32_to_bf16(a), f32_to_bf16(b), f32_to_bf16(c), f32_to_bf16(d)};
 }
 
-__device__ __forceinline__ float silu_f(float x) { return x / (1.0f + __expf(-x)); }
+// Both activations are evaluated as x / (1 + 2^a) with the hardware exp2
+// and reciprocal (a few instructions instead of the library tanh); the
+// tanh-form GELU uses 0.5 (1 + tanh(u)) = 1 / (1 + exp(-2u)).
+__device__ __forceinline__ float silu_f(float x) {
+  return __fdividef(x, 1.0f + exp2f(-1.4426950408889634f * x));
+}
 __device__ __forceinline__ float gelu_tanh_f(float x) {
-  const float c = 0.7978845608028654f;  // sqrt(2/pi)
-  return 0.5f * x * (1.0f + tanhf(c * (x + 0.044715f * x * x * x)));
+  const float c = -2.0f * 0.7978845608028654f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
+  return __fdividef(x, 1.0f + exp2f(c * fmaf(0.044715f * x, x * x, x)));
 }
 
 // ------------------------------------------------------------ GEMM launches
