@@ -33,6 +33,8 @@
 // Paired epilogues rely on the weight packing: columns [64p, 64p+32) and
 // [64p+32, 64p+64) of a packed matrix hold the two partners of a pair, which
 // then sit in the same lane and register of two adjacent 32-column tiles.
+#include <type_traits>
+
 #include "fv_internal.h"
 
 namespace fv {
@@ -91,13 +93,13 @@ __device__ __forceinline__ void tile_of(int& tm, int& tn) {
   tn = i / gm;
 }
 
-template <typename T, int BM, int BN, int NW, int WGM, class Epi>
-__global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ A,
-                                                       const T* __restrict__ Bt, int M, int N,
-                                                       int K, int KS, float* __restrict__ ws,
-                                                       Epi epi) {
+template <typename T, int BM, int BN, int NW, int WGM, int KG, class Epi>
+__global__ __launch_bounds__(64 * NW * KG) void gemm_kernel(const T* __restrict__ A,
+                                                            const T* __restrict__ Bt, int M,
+                                                            int N, int K, int KS,
+                                                            float* __restrict__ ws, Epi epi) {
   using MF = Mf32<T>;
-  constexpr int NT = 64 * NW;
+  constexpr int NT = 64 * NW * KG;
   constexpr int WGN = NW / WGM;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int FM = WTM / 32, FN = WTN / 32;
@@ -105,14 +107,18 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ A,
   constexpr int BK = 8 * EPV;               // 128 bytes of k per row and stage
   constexpr int LDR = BK + EPV;             // LDS row pitch (one vector of padding)
   constexpr int NA = BM * 8 / NT, NB = BN * 8 / NT, NP = NA + NB;  // 16-byte pieces per thread
-  constexpr int NSTEP = BK / MF::KM;
+  constexpr int NSTEP = BK / MF::KM;        // k-steps per stage
+  constexpr int NSG = NSTEP / KG;           // k-steps of a stage per wave group
   static_assert(FM >= 1 && FN >= 1 && WGM * WGN == NW, "bad tile");
-  static_assert((BM * 8) % NT == 0 && (BN * 8) % NT == 0 && NSTEP % 2 == 0, "bad tile");
+  static_assert((BM * 8) % NT == 0 && (BN * 8) % NT == 0 && NSG % 2 == 0, "bad tile");
+  static_assert(KG == 1 || NW * FM * FN * 4096 <= 2 * (BM + BN) * LDR * (int)sizeof(T),
+                "k-group reduction does not fit the staging buffers");
 
   __shared__ __attribute__((aligned(16))) T sm[2 * (BM + BN) * LDR];  // [buf][A rows ; B rows]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave % WGM, wn = wave / WGM;
+  const int kg = wave / NW, wv = wave - kg * NW;  // k-group; wave within the group
+  const int wm = wv % WGM, wn = wv / WGM;
   int tm, tn;
   tile_of(tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
@@ -156,10 +162,14 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ A,
 
   // Fragments are double-buffered: those of k-step ks+1 are read while the
   // MFMAs of k-step ks run.  The next stage's register pieces go to the
-  // other LDS buffer during k-steps 0..NSTEP-2 (each freed register then
-  // loads its piece of the stage after that); one barrier, placed before the
-  // last k-step, publishes the new stage, whose first fragments are read
-  // while the last k-step's MFMAs run.
+  // other LDS buffer during a group's k-steps 0..NSG-2 (each freed register
+  // then loads its piece of the stage after that); one barrier, placed
+  // before the group's last k-step, publishes the new stage, whose first
+  // fragments are read while the last k-step's MFMAs run.  With KG = 2 the
+  // two wave groups take the first and second half of every stage's k-steps
+  // on the same output tile (twice the waves per CU, and so twice the LDS
+  // requests in flight, for the same LDS bytes) and their accumulators are
+  // summed through LDS at the end.
   const int lr = lane & 31, lk = MF::KG * (lane >> 5);
   typename MF::frag af[2][FM], bfr[2][FN];
   auto read_frags = [&](int slot, int buf, int ks) __attribute__((always_inline)) {
@@ -169,19 +179,20 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ A,
 #pragma unroll
     for (int j = 0; j < FN; ++j) bfr[slot][j] = MF::load(base + (brow + 32 * j + lr) * LDR);
   };
-  read_frags(0, 0, 0);
+  const int s0 = kg * NSG;
+  read_frags(0, 0, s0);
   for (int kt = kt0; kt < kt1; ++kt) {
     const int cur = (kt - kt0) & 1;
     const int knext = min((kt + 2) * BK, klast);  // unconditional prefetch (clamped)
     T* const nxt = sm + (cur ^ 1) * (BM + BN) * LDR;
 #pragma unroll
-    for (int ks = 0; ks < NSTEP; ++ks) {
+    for (int ks = 0; ks < NSG; ++ks) {
       const int cb = ks & 1;
-      if (ks + 1 < NSTEP) {
-        read_frags(cb ^ 1, cur, ks + 1);
+      if (ks + 1 < NSG) {
+        read_frags(cb ^ 1, cur, s0 + ks + 1);
       } else {
         __syncthreads();
-        read_frags(cb ^ 1, cur ^ 1, 0);
+        read_frags(cb ^ 1, cur ^ 1, s0);
       }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
@@ -190,7 +201,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ A,
       int nw = 0;
 #pragma unroll
       for (int p = 0; p < NP; ++p) {
-        if (ks + 1 == NSTEP || (p * (NSTEP - 1)) / NP != ks) continue;
+        if (ks + 1 == NSG || (p * (NSG - 1)) / NP != ks) continue;
         *reinterpret_cast<u32x4*>(&nxt[lp[p]]) = rg[p];
         rg[p] = *reinterpret_cast<const u32x4*>(gp[p] + knext);
         ++nw;
@@ -216,6 +227,40 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ A,
         if (q >= nrd + nw) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     }
   }
+  if constexpr (KG > 1) {
+    // group kg > 0 hands its sums to group 0 through the (now idle) staging
+    // buffers: [wave][i][j][register quad][lane][4], 16 bytes per lane
+    __syncthreads();
+    f32x4* red = reinterpret_cast<f32x4*>(sm);
+    for (int g = 1; g < KG; ++g) {
+      if (kg == g) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              red[(((wv * FM + i) * FN + j) * 4 + q) * 64 + lane] =
+                  f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                        acc[i][j][4 * q + 3]};
+      }
+      __syncthreads();
+      if (kg == 0) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const f32x4 v = red[(((wv * FM + i) * FN + j) * 4 + q) * 64 + lane];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] += v[e];
+            }
+      }
+      if (g + 1 < KG) __syncthreads();
+    }
+    if (kg != 0) return;
+  }
   const int ar = wm * WTM, bc = wn * WTN;
 
   if (KS > 1) {
@@ -236,6 +281,129 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ A,
     return;
   }
   epi.template apply<FM, FN>(acc, m0 + ar, n0 + bc, lane, M);
+}
+
+// ---------------------------------------------------------- large-M bf16 GEMM
+// 256x256 output tile, 8 waves (2 per SIMD) with 128x64 wave tiles.  The
+// k-tiles (64 k = 128 bytes per row of A and W) go from memory straight to
+// LDS with the direct-to-LDS loads (no staging registers, no LDS store
+// instructions) into two buffers; 16-byte piece c of stage row r sits at
+// piece c ^ ((r / 2) % 8), which keeps the MFMA fragment reads conflict-free
+// without padding.  Tile kt + 2 is requested at the single barrier of k-tile
+// kt, right after every wave has read its last fragments of kt.
+constexpr int kBigBM = 256, kBigBN = 256, kBigWaves = 8, kBigWGM = 2;
+constexpr int kBigLds = 2 * (kBigBM + kBigBN) * 128;
+
+__device__ __forceinline__ void lds_dma16(const void* src, void* lds) {
+  __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {  // at most N vector memory ops outstanding
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+__device__ __forceinline__ void wait_lgkmcnt0() {
+  __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));
+}
+
+template <class Epi>
+__global__ __launch_bounds__(64 * kBigWaves) void gemm_big_kernel(const bf16_t* __restrict__ A,
+                                                                  const bf16_t* __restrict__ Bt,
+                                                                  int M, int N, int K, Epi epi) {
+  constexpr int BM = kBigBM, BN = kBigBN, NW = kBigWaves, WGM = kBigWGM;
+  constexpr int WGN = NW / WGM, WTM = BM / WGM, WTN = BN / WGN, FM = WTM / 32, FN = WTN / 32;
+  constexpr int BK = 64, NSTEP = 4;
+  constexpr int STAGE = (BM + BN) * 128;            // bytes
+  constexpr int NI = (BM + BN) * 8 / (64 * NW);      // direct loads per wave per stage
+  extern __shared__ __attribute__((aligned(16))) bf16_t big_smem[];
+  unsigned char* smem = reinterpret_cast<unsigned char*>(big_smem);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave % WGM, wn = wave / WGM;
+  int tm, tn;
+  tile_of(tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int nk = K / BK;
+
+  // lane's piece of each of the wave's loads: 16-byte unit p of a stage
+  const bf16_t* src[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int p = 64 * (NI * wave + i) + lane;
+    const int r = p >> 3, c = (p & 7) ^ ((r >> 1) & 7);
+    src[i] = r < BM ? A + (size_t)min(m0 + r, M - 1) * K + 8 * c
+                    : Bt + (size_t)(n0 + r - BM) * K + 8 * c;
+  }
+  auto issue = [&](int kt, int stage) __attribute__((always_inline)) {
+    unsigned char* st = smem + stage * STAGE + 1024 * NI * wave;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) lds_dma16(src[i] + (size_t)kt * BK, st + 1024 * i);
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
+  const int lr = lane & 31, lg = lane >> 5;
+  const int swz = (lr >> 1) & 7;  // rows 32 i + lr of any fragment share it
+  const int arow = wm * WTM, brow = BM + wn * WTN;
+  u32x4 af[2][FM], bfr[2][FN];
+  auto read_frags = [&](int slot, int stage, int ks) __attribute__((always_inline)) {
+    const bf16_t* st = reinterpret_cast<const bf16_t*>(smem + stage * STAGE);
+    const int co = 8 * ((2 * ks + lg) ^ swz);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+      af[slot][i] = *reinterpret_cast<const u32x4*>(st + (arow + 32 * i + lr) * 64 + co);
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+      bfr[slot][j] = *reinterpret_cast<const u32x4*>(st + (brow + 32 * j + lr) * 64 + co);
+  };
+
+  issue(0, 0);
+  if (nk > 1) {
+    issue(1, 1);
+    wait_vmcnt<NI>();
+  } else {
+    wait_vmcnt<0>();
+  }
+  __builtin_amdgcn_s_barrier();
+  read_frags(0, 0, 0);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+#pragma unroll
+    for (int ks = 0; ks < NSTEP; ++ks) {
+      const int cb = ks & 1;
+      if (ks + 1 < NSTEP) {
+        read_frags(cb ^ 1, cur, ks + 1);
+      } else {
+        // this wave's loads of tile kt + 1 landed and its reads of tile kt
+        // completed; after the barrier both hold for every wave
+        wait_vmcnt<0>();
+        wait_lgkmcnt0();
+        __builtin_amdgcn_s_barrier();
+        if (kt + 2 < nk) issue(kt + 2, cur);
+        if (kt + 1 < nk) read_frags(cb ^ 1, cur ^ 1, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8, af[cb][i]), __builtin_bit_cast(bf16x8, bfr[cb][j]),
+              acc[i][j], 0, 0, 0);
+      if (ks + 1 < NSTEP) {  // one fragment read after each MFMA
+#pragma unroll
+        for (int q = 0; q < FM + FN; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+#pragma unroll
+        for (int q = FM + FN; q < FM * FN; ++q) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      }
+    }
+  }
+  epi.template apply<FM, FN>(acc, m0 + arow, n0 + wn * WTN, lane, M);
 }
 
 // Sum of the KS split partials of each tile, in split order, followed by the
@@ -458,23 +626,47 @@ struct EpiGelu {
   }
 };
 
+// Raw split partials only (no epilogue, no reduction); the caller reduces them.
+struct EpiNone {
+  template <int FM, int FN>
+  __device__ void apply(f32x16 (&)[FM][FN], int, int, int, int) const {}
+};
+
 // -------------------------------------------------------------- tile choice
 // Tile shapes (BM x BN, waves); every wave owns a sub-tile at least 64
 // columns wide, so paired epilogues find both partners of a 64-column pair
 // group in one wave.
-enum Tile { T256x128w8 = 0, T128x128w8 = 1, T64x128w4 = 2, T32x128w2 = 3 };
-constexpr int kTileBM[] = {256, 128, 64, 32};
-constexpr int kTileBN[] = {128, 128, 128, 128};
+enum Tile { T256x128w8 = 0, T128x128w8 = 1, T64x128w4 = 2, T32x128w2 = 3, T256x256big = 4 };
+constexpr int kTileBM[] = {256, 128, 64, 32, 256};
+constexpr int kTileBN[] = {128, 128, 128, 128, 256};
+// k-groups per tile (waves per block = NW x KG): the 2-wave 32-row tile
+// (M <= 32: weight-streaming GEMMs) gets a second wave group, doubling the
+// loads and LDS reads in flight; the larger tiles measured no gain.
+constexpr int kTileKG[] = {1, 1, 1, 2};
 
-template <typename T, int BM, int BN, int NW, int WGM, class Epi>
+template <typename T, int BM, int BN, int NW, int WGM, int KG, class Epi>
 void launch_tile(const T* A, const T* Bt, int M, int N, int K, const GemmPlan& p,
                  const GemmWork& w, const Epi& epi, hipStream_t s) {
   dim3 grid(N / BN, (M + BM - 1) / BM, p.ks);
-  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, NW, WGM, Epi>), grid, dim3(64 * NW), 0, s, A, Bt, M,
-                     N, K, p.ks, w.ws, epi);
-  if (p.ks > 1)
+  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, NW, WGM, KG, Epi>), grid, dim3(64 * NW * KG), 0, s,
+                     A, Bt, M, N, K, p.ks, w.ws, epi);
+  if (p.ks > 1 && !std::is_same<Epi, EpiNone>::value)
     hipLaunchKernelGGL((gemm_reduce_kernel<BM, BN, NW, WGM, Epi>), dim3(grid.x, grid.y),
                        dim3(64 * NW), 0, s, w.ws, M, N, p.ks, epi);
+}
+
+template <class Epi>
+hipError_t allow_big_lds() {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_big_kernel<Epi>),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, kBigLds);
+}
+
+template <class Epi>
+void launch_big(const bf16_t* A, const bf16_t* Bt, int M, int N, int K, const Epi& epi,
+                hipStream_t s) {
+  dim3 grid(N / kBigBN, (M + kBigBM - 1) / kBigBM);
+  hipLaunchKernelGGL((gemm_big_kernel<Epi>), grid, dim3(64 * kBigWaves), kBigLds, s, A, Bt, M, N,
+                     K, epi);
 }
 
 template <typename T, class Epi>
@@ -482,11 +674,17 @@ void run_gemm(const T* A, const T* Bt, int M, int N, int K, const GemmWork& w, c
               hipStream_t s) {
   if (M <= 0) return;
   const GemmPlan p = plan_gemm(M, N, K, sizeof(T) == 2);
+  if constexpr (sizeof(T) == 2) {
+    if (p.tile == T256x256big) {
+      launch_big(A, Bt, M, N, K, epi, s);
+      return;
+    }
+  }
   switch (p.tile) {
-    case T256x128w8: launch_tile<T, 256, 128, 8, 4>(A, Bt, M, N, K, p, w, epi, s); break;
-    case T128x128w8: launch_tile<T, 128, 128, 8, 4>(A, Bt, M, N, K, p, w, epi, s); break;
-    case T64x128w4: launch_tile<T, 64, 128, 4, 2>(A, Bt, M, N, K, p, w, epi, s); break;
-    case T32x128w2: launch_tile<T, 32, 128, 2, 1>(A, Bt, M, N, K, p, w, epi, s); break;
+    case T256x128w8: launch_tile<T, 256, 128, 8, 4, kTileKG[0]>(A, Bt, M, N, K, p, w, epi, s); break;
+    case T128x128w8: launch_tile<T, 128, 128, 8, 4, kTileKG[1]>(A, Bt, M, N, K, p, w, epi, s); break;
+    case T64x128w4: launch_tile<T, 64, 128, 4, 2, kTileKG[2]>(A, Bt, M, N, K, p, w, epi, s); break;
+    case T32x128w2: launch_tile<T, 32, 128, 2, 1, kTileKG[3]>(A, Bt, M, N, K, p, w, epi, s); break;
     default: break;  // N % 128 != 0 is rejected at fv_create
   }
 }
@@ -504,7 +702,7 @@ GemmPlan plan_gemm(int M, int N, int K, bool bf16) {
   const int bk = bf16 ? 64 : 32, nk = K / bk;
   auto ntiles = [&](int t) { return ((M + kTileBM[t] - 1) / kTileBM[t]) * (N / kTileBN[t]); };
   if (M >= 4096)
-    p.tile = T256x128w8;
+    p.tile = bf16 && N % 256 == 0 ? T256x256big : T256x128w8;
   else if (M > 256)
     p.tile = ntiles(T128x128w8) >= 200 ? T128x128w8 : T64x128w4;
   else if (M > 32)
@@ -514,7 +712,7 @@ GemmPlan plan_gemm(int M, int N, int K, bool bf16) {
   const int bm = kTileBM[p.tile], bn = kTileBN[p.tile];
   p.tiles = ntiles(p.tile);
   p.ks = 1;
-  if (p.tiles < 128)
+  if (p.tiles < 128 && p.tile != T256x256big)
     while ((long)p.tiles * p.ks * 2 <= 320 && nk / (p.ks * 2) >= 4 && p.ks < 8) p.ks *= 2;
   p.ws_floats = p.ks > 1 ? (size_t)p.ks * M * N : 0;
   (void)bm;
@@ -522,11 +720,6 @@ GemmPlan plan_gemm(int M, int N, int K, bool bf16) {
   return p;
 }
 
-// Raw split partials only (no epilogue); the caller reduces them.
-struct EpiNone {
-  template <int FM, int FN>
-  __device__ void apply(f32x16 (&)[FM][FN], int, int, int, int) const {}
-};
 
 template <typename T>
 int gemm_partials(const T* A, const T* Bt, int M, int N, int K, const GemmWork& w,
@@ -534,29 +727,10 @@ int gemm_partials(const T* A, const T* Bt, int M, int N, int K, const GemmWork& 
   const GemmPlan p = plan_gemm(M, N, K, sizeof(T) == 2);
   if (p.ks <= 1) return 1;
   switch (p.tile) {
-    case T256x128w8: {
-      dim3 g(N / 128, (M + 255) / 256, p.ks);
-      hipLaunchKernelGGL((gemm_kernel<T, 256, 128, 8, 4, EpiNone>), g, dim3(512), 0, s, A, Bt, M, N,
-                         K, p.ks, w.ws, EpiNone{});
-      break;
-    }
-    case T128x128w8: {
-      dim3 g(N / 128, (M + 127) / 128, p.ks);
-      hipLaunchKernelGGL((gemm_kernel<T, 128, 128, 8, 4, EpiNone>), g, dim3(512), 0, s, A, Bt, M, N,
-                         K, p.ks, w.ws, EpiNone{});
-      break;
-    }
-    case T64x128w4: {
-      dim3 g(N / 128, (M + 63) / 64, p.ks);
-      hipLaunchKernelGGL((gemm_kernel<T, 64, 128, 4, 2, EpiNone>), g, dim3(256), 0, s, A, Bt, M, N,
-                         K, p.ks, w.ws, EpiNone{});
-      break;
-    }
-    default: {
-      dim3 g(N / 128, (M + 31) / 32, p.ks);
-      hipLaunchKernelGGL((gemm_kernel<T, 32, 128, 2, 1, EpiNone>), g, dim3(128), 0, s, A, Bt, M, N,
-                         K, p.ks, w.ws, EpiNone{});
-    }
+    case T256x128w8: launch_tile<T, 256, 128, 8, 4, kTileKG[0]>(A, Bt, M, N, K, p, w, EpiNone{}, s); break;
+    case T128x128w8: launch_tile<T, 128, 128, 8, 4, kTileKG[1]>(A, Bt, M, N, K, p, w, EpiNone{}, s); break;
+    case T64x128w4: launch_tile<T, 64, 128, 4, 2, kTileKG[2]>(A, Bt, M, N, K, p, w, EpiNone{}, s); break;
+    default: launch_tile<T, 32, 128, 2, 1, kTileKG[3]>(A, Bt, M, N, K, p, w, EpiNone{}, s);
   }
   return p.ks;
 }
@@ -591,6 +765,17 @@ template <typename T>
 void gemm_gelu(const T* A, const T* Bt, T* out, int M, int N, int K, const GemmWork& w,
                hipStream_t s) {
   run_gemm(A, Bt, M, N, K, w, EpiGelu<T>{out, N}, s);
+}
+
+// The large-M kernel's dynamic LDS exceeds the default limit; every
+// epilogue instantiation is raised once per device before any launch.
+hipError_t gemm_prepare() {
+  const hipError_t e[] = {allow_big_lds<EpiBiasSilu<bf16_t>>(), allow_big_lds<EpiBiasF32>(),
+                          allow_big_lds<EpiQkv<bf16_t>>(),      allow_big_lds<EpiGatedResid>(),
+                          allow_big_lds<EpiGeglu<bf16_t>>(),    allow_big_lds<EpiGelu<bf16_t>>()};
+  for (hipError_t x : e)
+    if (x != hipSuccess) return x;
+  return hipSuccess;
 }
 
 #define FV_INSTANTIATE(T)                                                                        \

@@ -134,6 +134,9 @@ void gemm_geglu(const T* A, const T* Bt, T* out, int M, int N, int K, const Gemm
 template <typename T>
 void gemm_gelu(const T* A, const T* Bt, T* out, int M, int N, int K, const GemmWork& w,
                hipStream_t s);
+// Raises the dynamic LDS limit of the large-M GEMM kernels (call once per
+// device before the first GEMM launch).
+hipError_t gemm_prepare();
 // Split-K GEMM that only writes its fp32 partials [KS][M][N] to w.ws; returns
 // KS, or 1 (nothing launched) when the plan does not split k.
 template <typename T>

@@ -54,6 +54,24 @@ def test_velocity_parity_batched64_sampled_streams():
         case.close()
 
 
+def test_velocity_parity_ragged_large_m():
+    """9 streams of the batched workload: 4500 token rows, so the large-row
+    GEMM tiles (256 rows) end in a partial tile of 148 rows, which belongs to
+    the last stream."""
+    w = synth.workload("batched64").replace(name="batched9", batch=9)
+    case = Case(w)
+    try:
+        v = case.gpu_velocity()
+        assert np.all(np.isfinite(v))
+        for b in (w.batch - 1, int(np.argmin(case.lens))):
+            ref = case.oracle_velocity(b)
+            errs = [rel_err(v[b, k], ref[k]) for k in range(w.n_chunks)]
+            _say(f"batched9 stream {b} (P={case.lens[b]}): max rel err {max(errs):.2e}")
+            assert max(errs) < tol(w), (b, errs)
+    finally:
+        case.close()
+
+
 def test_decode_steps_lockstep_pi05():
     """Two steps of the headline workload: emitted chunk within tolerance of
     the oracle, shifted slots bit-exact against the fp32 queue update of the
