@@ -1,4 +1,6 @@
 // Element-wise and row-wise kernels of the decode step.
+#include <algorithm>
+
 #include "fv_internal.h"
 
 namespace fv {
@@ -40,6 +42,9 @@ __global__ void time_embed_kernel(const float* __restrict__ t, T* __restrict__ e
 // of every row, reads w_in once for all rows in batches of independent
 // loads and keeps the x rows in LDS.
 constexpr int kEmbRows = 8;
+// Row counts from which the embedding and the velocity head switch to their
+// weights-in-registers variants, and the block count those aim for.
+constexpr int kManyRows = 4096, kRowBlocks = 512;
 
 __device__ __forceinline__ float block_sum_256(float v, float* red) {
   v = wave_sum(v);
@@ -138,6 +143,71 @@ __global__ __launch_bounds__(256) void embed_adarms_kernel(
                 hv[1] * rinv * (1.0f + sv[i][r][1]) + bv[i][r][1],
                 hv[2] * rinv * (1.0f + sv[i][r][2]) + bv[i][r][2],
                 hv[3] * rinv * (1.0f + sv[i][r][3]) + bv[i][r][3]);
+    }
+  }
+}
+
+// Many rows (W <= 1024, A <= 32): thread t keeps its four columns of w_in in
+// registers and the block runs batches of kEmbRows rows through them, so
+// w_in is read once per block instead of once per batch.
+template <typename T>
+__global__ __launch_bounds__(256) void embed_adarms_rows_kernel(
+    const float* __restrict__ x, const float* __restrict__ w_in, const float* __restrict__ b_in,
+    float* __restrict__ h, const float* __restrict__ mod, int mod_ld, int chunk_len, float eps,
+    T* __restrict__ u, int rows, int A, int W, int rows_per_block) {
+  __shared__ float sx[32][kEmbRows];
+  __shared__ float sred[kEmbRows][4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = 4 * tid;
+  const bool ok = c < W;
+  const f32x4 zero4 = f32x4{0.f, 0.f, 0.f, 0.f};
+  f32x4 wv[32];
+#pragma unroll
+  for (int a = 0; a < 32; ++a)
+    wv[a] = ok && a < A ? *reinterpret_cast<const f32x4*>(w_in + (size_t)a * W + c) : zero4;
+  const f32x4 bias = ok ? *reinterpret_cast<const f32x4*>(b_in + c) : zero4;
+  const int rend = min(rows, (blockIdx.x + 1) * rows_per_block);
+  for (int row0 = blockIdx.x * rows_per_block; row0 < rend; row0 += kEmbRows) {
+    __syncthreads();  // previous batch done with sx and sred
+    {  // entries a >= A are zero (their weights are zero too)
+      const int r = tid >> 5, a = tid & 31;
+      sx[a][r] = row0 + r < rend && a < A ? x[(size_t)(row0 + r) * A + a] : 0.f;
+    }
+    __syncthreads();
+    f32x4 acc[kEmbRows];
+#pragma unroll
+    for (int r = 0; r < kEmbRows; ++r) acc[r] = bias;
+#pragma unroll
+    for (int a = 0; a < 32; ++a) {
+#pragma unroll
+      for (int r = 0; r < kEmbRows; ++r) acc[r] += sx[a][r] * wv[a];
+      if ((a & 7) == 7) __builtin_amdgcn_sched_barrier(0);  // bounds the LDS reads in flight
+    }
+    float ss[kEmbRows];
+#pragma unroll
+    for (int r = 0; r < kEmbRows; ++r) {
+      ss[r] = acc[r][0] * acc[r][0] + acc[r][1] * acc[r][1] + acc[r][2] * acc[r][2] +
+              acc[r][3] * acc[r][3];
+      if (ok && row0 + r < rend) *reinterpret_cast<f32x4*>(h + (size_t)(row0 + r) * W + c) = acc[r];
+    }
+#pragma unroll
+    for (int r = 0; r < kEmbRows; ++r) {
+      const float v = wave_sum(ok ? ss[r] : 0.f);
+      if (lane == 0) sred[r][wave] = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kEmbRows; ++r) {
+      const int row = row0 + r;
+      if (row >= rend || !ok) break;
+      const float tot = sred[r][0] + sred[r][1] + sred[r][2] + sred[r][3];
+      const float rinv = 1.0f / sqrtf(tot / (float)W + eps);
+      const float* sc = mod + (size_t)(row / chunk_len) * mod_ld;
+      const f32x4 sv = *reinterpret_cast<const f32x4*>(sc + c);
+      const f32x4 bv = *reinterpret_cast<const f32x4*>(sc + W + c);
+      store4<T>(u + (size_t)row * W + c, acc[r][0] * rinv * (1.0f + sv[0]) + bv[0],
+                acc[r][1] * rinv * (1.0f + sv[1]) + bv[1], acc[r][2] * rinv * (1.0f + sv[2]) + bv[2],
+                acc[r][3] * rinv * (1.0f + sv[3]) + bv[3]);
     }
   }
 }
@@ -318,6 +388,87 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ h,
       float tot = b_out[aa];
       for (int p = 0; p < parts; ++p) tot += sp[(p * kFinalRows + r) * A + aa];
       v[(size_t)(row0 + r) * A + aa] = tot;
+    }
+  }
+}
+
+// Many rows (W <= 1024, A <= 32): 512 threads; thread (part, a) keeps its
+// contiguous slice (at most 64 entries) of column a of w_out in registers
+// and the block runs batches of 8 rows (one per wave) through it: w_out is
+// read once per block.  Slices are added in a fixed order, as in final_kernel.
+constexpr int kFinalRowsBig = 8;
+__global__ __launch_bounds__(512) void final_rows_kernel(const float* __restrict__ h,
+                                                         const float* __restrict__ mod, int mod_ld,
+                                                         int scale_off, int chunk_len, float eps,
+                                                         const float* __restrict__ w_out,
+                                                         const float* __restrict__ b_out,
+                                                         float* __restrict__ v, int rows, int W,
+                                                         int A, int rows_per_block) {
+  constexpr int R = kFinalRowsBig, KR = 64, NPL = 1024 / 64;
+  extern __shared__ float smem[];  // su [R][W], sp [parts][R][A]
+  float* su = smem;
+  float* sp = su + R * W;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, tid = threadIdx.x;
+  const int parts = 512 / A;
+  const int part = tid / A, a = tid - part * A;
+  const int kr = (((W + parts - 1) / parts) + 3) & ~3;  // multiple of 4, at most KR
+  const int k0 = part * kr, k1 = min(W, k0 + kr);
+  float wr[KR];
+#pragma unroll
+  for (int j = 0; j < KR; ++j) wr[j] = part < parts && k0 + j < k1 ? w_out[(size_t)(k0 + j) * A + a] : 0.f;
+  const int rend = min(rows, (blockIdx.x + 1) * rows_per_block);
+  for (int row0 = blockIdx.x * rows_per_block; row0 < rend; row0 += R) {
+    {
+      const int row = min(row0 + wave, rend - 1);
+      const float* hr = h + (size_t)row * W;
+      const float* sc = mod + (size_t)(row / chunk_len) * mod_ld + scale_off;
+      float hv[NPL], sv[NPL], bv[NPL];
+#pragma unroll
+      for (int i = 0; i < NPL; ++i) {
+        const int cc = lane + 64 * i;
+        hv[i] = cc < W ? hr[cc] : 0.f;
+        sv[i] = cc < W ? sc[cc] : 0.f;
+        bv[i] = cc < W ? sc[W + cc] : 0.f;
+      }
+      float ss = 0.f;
+#pragma unroll
+      for (int i = 0; i < NPL; ++i) ss += hv[i] * hv[i];
+      ss = wave_sum(ss);
+      const float rinv = 1.0f / sqrtf(ss / (float)W + eps);
+      __syncthreads();  // previous batch done with su and sp
+#pragma unroll
+      for (int i = 0; i < NPL; ++i) {
+        const int cc = lane + 64 * i;
+        if (cc < W) su[wave * W + cc] = hv[i] * rinv * (1.0f + sv[i]) + bv[i];
+      }
+    }
+    __syncthreads();
+    if (part < parts) {
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        float acc = 0.f;
+#pragma unroll
+        for (int j = 0; j < KR; j += 4) {
+          // past the slice: zero weights; the LDS value is replaced too, as it
+          // may be any bit pattern (the allocation is large enough to read)
+          const f32x4 x4 = k0 + j < k1 ? *reinterpret_cast<const f32x4*>(su + r * W + k0 + j)
+                                       : f32x4{0.f, 0.f, 0.f, 0.f};
+          acc = fmaf(x4[0], wr[j], acc);
+          acc = fmaf(x4[1], wr[j + 1], acc);
+          acc = fmaf(x4[2], wr[j + 2], acc);
+          acc = fmaf(x4[3], wr[j + 3], acc);
+        }
+        sp[(part * R + r) * A + a] = acc;
+      }
+    }
+    __syncthreads();
+    if (tid < R * A) {
+      const int r = tid / A, aa = tid - r * A;
+      if (row0 + r < rend) {
+        float tot = b_out[aa];
+        for (int p = 0; p < parts; ++p) tot += sp[(p * R + r) * A + aa];
+        v[(size_t)(row0 + r) * A + aa] = tot;
+      }
     }
   }
 }
@@ -535,6 +686,12 @@ template <typename T>
 void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, float* h,
                          const float* mod, int mod_ld, int chunk_len, float eps, T* u, int rows,
                          int A, int W, hipStream_t s) {
+  if (rows >= kManyRows && W <= 1024 && A <= 32) {
+    const int rpb = kEmbRows * std::max(1, rows / (kEmbRows * kRowBlocks));
+    hipLaunchKernelGGL((embed_adarms_rows_kernel<T>), dim3((rows + rpb - 1) / rpb), dim3(256), 0, s,
+                       x, w_in, b_in, h, mod, mod_ld, chunk_len, eps, u, rows, A, W, rpb);
+    return;
+  }
   const dim3 grid((rows + kEmbRows - 1) / kEmbRows);
   if (W <= 1024)
     hipLaunchKernelGGL((embed_adarms_kernel<T, 1>), grid, dim3(256), 0, s, x, w_in, b_in, h, mod,
@@ -568,6 +725,14 @@ void launch_final(const float* h, const float* mod, int mod_ld, int scale_off, i
                   float eps, const float* w_out, const float* b_out, float* v, int rows, int W,
                   int A, hipStream_t s) {
   const size_t lds = (size_t)(kFinalRows * W + 256 * kFinalRows) * sizeof(float);
+  if (rows >= kManyRows && W <= 1024 && W % 4 == 0 && A <= 32 && 4 * A <= 512 &&
+      ((((W + 512 / A - 1) / (512 / A)) + 3) & ~3) <= 64) {
+    const int rpb = kFinalRowsBig * std::max(1, rows / (kFinalRowsBig * kRowBlocks));
+    const size_t lds2 = (size_t)(kFinalRowsBig * W + 512 * kFinalRowsBig) * sizeof(float);
+    hipLaunchKernelGGL(final_rows_kernel, dim3((rows + rpb - 1) / rpb), dim3(512), lds2, s, h, mod,
+                       mod_ld, scale_off, chunk_len, eps, w_out, b_out, v, rows, W, A, rpb);
+    return;
+  }
   hipLaunchKernelGGL(final_kernel, dim3((rows + kFinalRows - 1) / kFinalRows), dim3(256), lds, s, h, mod, mod_ld,
                      scale_off, chunk_len, eps, w_out, b_out, v, rows, W, A);
 }
