@@ -328,6 +328,26 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 // O^T += V^T P^T with the MFMA's k index 8 g + e standing for key
 // 4 g + e (e < 4) or 16 + 4 g + e - 4 (e >= 4), and the V^T fragment reads
 // the same two 4-key runs.
+// (row tile, stream x kv head) of this block.  Block b runs on die b % 8 of
+// the chip (each die has its own L2); on large grids without key splits the
+// blocks of a die take a contiguous range of the (stream-major) work list,
+// so the row tiles of one stream, which read the same keys and values, run
+// together on one die instead of being spread over all eight.
+__device__ __forceinline__ void attn_block_of(int& rtile, int& bg) {
+  const int nx = gridDim.x, nb = nx * gridDim.y;
+  if (gridDim.z > 1 || nb < 64) {
+    rtile = blockIdx.x;
+    bg = blockIdx.y;
+    return;
+  }
+  const int blk = blockIdx.y * nx + blockIdx.x;
+  const int per = nb >> 3, rem = nb & 7;
+  const int x = blk & 7, slot = blk >> 3;
+  const int L = x * per + min(x, rem) + slot;
+  bg = L / nx;
+  rtile = L - bg * nx;
+}
+
 template <int DH, int NWV>
 __global__ __launch_bounds__(64 * NWV) void attn16_kernel(AttnArgs a) {
   using T = bf16_t;
@@ -345,8 +365,10 @@ __global__ __launch_bounds__(64 * NWV) void attn16_kernel(AttnArgs a) {
 
   const int G = a.n_q_heads / a.n_kv_heads;
   const int rows_bg = a.tokens * G;
-  const int tile0 = blockIdx.x * RB;
-  const int b = blockIdx.y / a.n_kv_heads, g = blockIdx.y - b * a.n_kv_heads;
+  int rtile, bg;
+  attn_block_of(rtile, bg);
+  const int tile0 = rtile * RB;
+  const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
   const int split = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int P = a.len[b];
