@@ -283,17 +283,21 @@ __global__ __launch_bounds__(64 * NW * KG) void gemm_kernel(const T* __restrict_
   epi.template apply<FM, FN>(acc, m0 + ar, n0 + bc, lane, M);
 }
 
-// ---------------------------------------------------------- large-M bf16 GEMM
-// 256x256 output tile, 8 waves (2 per SIMD) with 128x64 wave tiles.  The
-// k-tiles (64 k = 128 bytes per row of A and W) go from memory straight to
-// LDS with the direct-to-LDS loads (no staging registers, no LDS store
-// instructions) into two buffers; 16-byte piece c of stage row r sits at
-// piece c ^ ((r / 2) % 8), which keeps the MFMA fragment reads conflict-free
-// without padding.  Tile kt + 2 is requested at the single barrier of k-tile
-// kt, right after every wave has read its last fragments of kt.
-constexpr int kBigBM = 256, kBigBN = 256, kBigWaves = 8, kBigWGM = 2;
-constexpr int kBigLds = 2 * (kBigBM + kBigBN) * 128;
-
+// ------------------------------------------------- direct-to-LDS bf16 GEMM
+// BM x BN output tile per block of NW waves (WGM along M).  The A and W
+// k-tiles (64 k = 128 bytes per row) go from memory straight to LDS with the
+// direct-to-LDS loads (no staging registers, no LDS store instructions) into
+// a ring of NS stages; 16-byte piece c of stage row r sits at piece
+// c ^ ((r / 2) % 8), which keeps the MFMA fragment reads conflict-free
+// without padding.  One barrier per k-tile, after every wave's last fragment
+// reads of the tile; the loads of tile k + NS are issued right after it into
+// the stage just consumed, so NS - 1 tiles are in flight while one is
+// multiplied.  Fragments of k-step s + 1 are read during the MFMAs of
+// k-step s.  Split-K (KS > 1) writes fp32 partials as gemm_kernel does.
+//   * 256x256, 8 waves (128x64 wave tiles), 2 stages: large M (batch 64);
+//   * 128x128, 8 waves and 64x128, 4 waves (32x64 wave tiles), 3 stages
+//     (2 on grids of several rounds): medium M (batch 1), where the deeper
+//     ring hides the load latency.
 __device__ __forceinline__ void lds_dma16(const void* src, void* lds) {
   __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
 }
@@ -305,17 +309,23 @@ __device__ __forceinline__ void wait_lgkmcnt0() {
   __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));
 }
 
-template <class Epi>
-__global__ __launch_bounds__(64 * kBigWaves) void gemm_big_kernel(const bf16_t* __restrict__ A,
-                                                                  const bf16_t* __restrict__ Bt,
-                                                                  int M, int N, int K, Epi epi) {
-  constexpr int BM = kBigBM, BN = kBigBN, NW = kBigWaves, WGM = kBigWGM;
+template <int BM, int BN, int NW, int WGM, int NS>
+constexpr int dma_lds_bytes() {
+  return NS * (BM + BN) * 128;
+}
+
+template <int BM, int BN, int NW, int WGM, int NS, class Epi>
+__global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(const bf16_t* __restrict__ A,
+                                                           const bf16_t* __restrict__ Bt, int M,
+                                                           int N, int K, int KS,
+                                                           float* __restrict__ ws, Epi epi) {
   constexpr int WGN = NW / WGM, WTM = BM / WGM, WTN = BN / WGN, FM = WTM / 32, FN = WTN / 32;
   constexpr int BK = 64, NSTEP = 4;
-  constexpr int STAGE = (BM + BN) * 128;            // bytes
-  constexpr int NI = (BM + BN) * 8 / (64 * NW);      // direct loads per wave per stage
-  extern __shared__ __attribute__((aligned(16))) bf16_t big_smem[];
-  unsigned char* smem = reinterpret_cast<unsigned char*>(big_smem);
+  constexpr int STAGE = (BM + BN) * 128;        // bytes
+  constexpr int NI = (BM + BN) * 8 / (64 * NW);  // direct loads per wave per stage
+  static_assert(NI * 64 * NW == (BM + BN) * 8 && FM >= 1 && FN >= 1 && NS >= 2, "bad tile");
+  extern __shared__ __attribute__((aligned(16))) bf16_t dma_smem[];
+  unsigned char* smem = reinterpret_cast<unsigned char*>(dma_smem);
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -323,7 +333,9 @@ __global__ __launch_bounds__(64 * kBigWaves) void gemm_big_kernel(const bf16_t* 
   int tm, tn;
   tile_of(tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
-  const int nk = K / BK;
+  const int nk_all = K / BK;
+  const int kz = blockIdx.z;
+  const int kt0 = (kz * nk_all) / KS, kt1 = ((kz + 1) * nk_all) / KS;
 
   // lane's piece of each of the wave's loads: 16-byte unit p of a stage
   const bf16_t* src[NI];
@@ -360,30 +372,35 @@ __global__ __launch_bounds__(64 * kBigWaves) void gemm_big_kernel(const bf16_t* 
       bfr[slot][j] = *reinterpret_cast<const u32x4*>(st + (brow + 32 * j + lr) * 64 + co);
   };
 
-  issue(0, 0);
-  if (nk > 1) {
-    issue(1, 1);
-    wait_vmcnt<NI>();
-  } else {
+#pragma unroll
+  for (int p = 0; p < NS; ++p)
+    if (kt0 + p < kt1) issue(kt0 + p, p);
+  if (kt1 - kt0 >= NS)
+    wait_vmcnt<(NS - 1) * NI>();  // tile kt0 landed, the next NS - 1 may be in flight
+  else
     wait_vmcnt<0>();
-  }
   __builtin_amdgcn_s_barrier();
   read_frags(0, 0, 0);
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
+  int stage = 0;
+  for (int kt = kt0; kt < kt1; ++kt) {
+    const int nstage = stage + 1 == NS ? 0 : stage + 1;
 #pragma unroll
     for (int ks = 0; ks < NSTEP; ++ks) {
       const int cb = ks & 1;
       if (ks + 1 < NSTEP) {
-        read_frags(cb ^ 1, cur, ks + 1);
+        read_frags(cb ^ 1, stage, ks + 1);
       } else {
-        // this wave's loads of tile kt + 1 landed and its reads of tile kt
-        // completed; after the barrier both hold for every wave
-        wait_vmcnt<0>();
+        // this wave's loads of tile kt + 1 landed (later ones may still fly)
+        // and its reads of tile kt completed; after the barrier both hold for
+        // every wave, and this stage is free for tile kt + NS
+        if (kt + NS - 1 < kt1)
+          wait_vmcnt<(NS - 2) * NI>();
+        else
+          wait_vmcnt<0>();
         wait_lgkmcnt0();
         __builtin_amdgcn_s_barrier();
-        if (kt + 2 < nk) issue(kt + 2, cur);
-        if (kt + 1 < nk) read_frags(cb ^ 1, cur ^ 1, 0);
+        if (kt + NS < kt1) issue(kt + NS, stage);
+        if (kt + 1 < kt1) read_frags(cb ^ 1, nstage, 0);
       }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
@@ -393,17 +410,35 @@ __global__ __launch_bounds__(64 * kBigWaves) void gemm_big_kernel(const bf16_t* 
               __builtin_bit_cast(bf16x8, af[cb][i]), __builtin_bit_cast(bf16x8, bfr[cb][j]),
               acc[i][j], 0, 0, 0);
       if (ks + 1 < NSTEP) {  // one fragment read after each MFMA
+        constexpr int nrd = FM + FN < FM * FN ? FM + FN : FM * FN;
 #pragma unroll
-        for (int q = 0; q < FM + FN; ++q) {
+        for (int q = 0; q < nrd; ++q) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
 #pragma unroll
-        for (int q = FM + FN; q < FM * FN; ++q) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        for (int q = nrd; q < FM * FN; ++q) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       }
     }
+    stage = nstage;
   }
-  epi.template apply<FM, FN>(acc, m0 + arow, n0 + wn * WTN, lane, M);
+  const int ar = wm * WTM, bc = wn * WTN;
+  if (KS > 1) {
+    float* part = ws + (size_t)kz * M * N;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = n0 + bc + 32 * j + lr;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + ar + 32 * i + acc_row(r, lane);
+          if (row < M) part[(size_t)row * N + col] = acc[i][j][r];
+        }
+      }
+    return;
+  }
+  epi.template apply<FM, FN>(acc, m0 + ar, n0 + bc, lane, M);
 }
 
 // Sum of the KS split partials of each tile, in split order, followed by the
@@ -440,6 +475,12 @@ __global__ __launch_bounds__(64 * NW) void gemm_reduce_kernel(const float* __res
 }
 
 // ----------------------------------------------------------------- epilogues
+// Raw split partials only (no epilogue, no reduction); the caller reduces them.
+struct EpiNone {
+  template <int FM, int FN>
+  __device__ void apply(f32x16 (&)[FM][FN], int, int, int, int) const {}
+};
+
 // Element (i, j, r) of a wave's accumulators sits at
 //   row = row0 + 32 i + acc_row(r, lane),   col = col0 + 32 j + lane % 32.
 
@@ -626,12 +667,6 @@ struct EpiGelu {
   }
 };
 
-// Raw split partials only (no epilogue, no reduction); the caller reduces them.
-struct EpiNone {
-  template <int FM, int FN>
-  __device__ void apply(f32x16 (&)[FM][FN], int, int, int, int) const {}
-};
-
 // -------------------------------------------------------------- tile choice
 // Tile shapes (BM x BN, waves); every wave owns a sub-tile at least 64
 // columns wide, so paired epilogues find both partners of a 64-column pair
@@ -655,18 +690,57 @@ void launch_tile(const T* A, const T* Bt, int M, int N, int K, const GemmPlan& p
                        dim3(64 * NW), 0, s, w.ws, M, N, p.ks, epi);
 }
 
-template <class Epi>
-hipError_t allow_big_lds() {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_big_kernel<Epi>),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, kBigLds);
+// Direct-to-LDS instances: (tile, waves, stages) of the bf16 tiles that use it.
+#define FV_DMA_TILES(X) \
+  X(256, 256, 8, 2, 2)  \
+  X(128, 128, 8, 4, 3)  \
+  X(128, 128, 8, 4, 2)  \
+  X(64, 128, 4, 2, 3)   \
+  X(64, 128, 4, 2, 2)
+
+template <int BM, int BN, int NW, int WGM, int NS, class Epi>
+hipError_t allow_dma_lds() {
+  return hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&gemm_dma_kernel<BM, BN, NW, WGM, NS, Epi>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, dma_lds_bytes<BM, BN, NW, WGM, NS>());
 }
 
+template <int BM, int BN, int NW, int WGM, int NS, class Epi>
+void launch_dma(const bf16_t* A, const bf16_t* Bt, int M, int N, int K, const GemmPlan& p,
+                const GemmWork& w, const Epi& epi, hipStream_t s) {
+  dim3 grid(N / BN, (M + BM - 1) / BM, p.ks);
+  hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, NW, WGM, NS, Epi>), grid, dim3(64 * NW),
+                     (dma_lds_bytes<BM, BN, NW, WGM, NS>()), s, A, Bt, M, N, K, p.ks, w.ws, epi);
+  if (p.ks > 1 && !std::is_same<Epi, EpiNone>::value)
+    hipLaunchKernelGGL((gemm_reduce_kernel<BM, BN, NW, WGM, Epi>), dim3(grid.x, grid.y),
+                       dim3(64 * NW), 0, s, w.ws, M, N, p.ks, epi);
+}
+
+// Launches tile p.tile with the direct-to-LDS kernel when it has one;
+// returns false otherwise.  Medium tiles take three stages when the grid is
+// about one round of the chip (the deeper ring hides load latency, measured
+// 1568 against 1864 us per batch-1 step with two), two stages when it is
+// many rounds (two workgroups then fit per CU and overlap each other).
 template <class Epi>
-void launch_big(const bf16_t* A, const bf16_t* Bt, int M, int N, int K, const Epi& epi,
-                hipStream_t s) {
-  dim3 grid(N / kBigBN, (M + kBigBM - 1) / kBigBM);
-  hipLaunchKernelGGL((gemm_big_kernel<Epi>), grid, dim3(64 * kBigWaves), kBigLds, s, A, Bt, M, N,
-                     K, epi);
+bool try_dma(const bf16_t* A, const bf16_t* Bt, int M, int N, int K, const GemmPlan& p,
+             const GemmWork& w, const Epi& epi, hipStream_t s) {
+  const bool rounds = (long)p.tiles * p.ks >= 512;
+  switch (p.tile) {
+    case T256x256big: launch_dma<256, 256, 8, 2, 2>(A, Bt, M, N, K, p, w, epi, s); return true;
+    case T128x128w8:
+      if (rounds)
+        launch_dma<128, 128, 8, 4, 2>(A, Bt, M, N, K, p, w, epi, s);
+      else
+        launch_dma<128, 128, 8, 4, 3>(A, Bt, M, N, K, p, w, epi, s);
+      return true;
+    case T64x128w4:
+      if (rounds)
+        launch_dma<64, 128, 4, 2, 2>(A, Bt, M, N, K, p, w, epi, s);
+      else
+        launch_dma<64, 128, 4, 2, 3>(A, Bt, M, N, K, p, w, epi, s);
+      return true;
+    default: return false;
+  }
 }
 
 template <typename T, class Epi>
@@ -675,10 +749,7 @@ void run_gemm(const T* A, const T* Bt, int M, int N, int K, const GemmWork& w, c
   if (M <= 0) return;
   const GemmPlan p = plan_gemm(M, N, K, sizeof(T) == 2);
   if constexpr (sizeof(T) == 2) {
-    if (p.tile == T256x256big) {
-      launch_big(A, Bt, M, N, K, epi, s);
-      return;
-    }
+    if (try_dma(A, Bt, M, N, K, p, w, epi, s)) return;
   }
   switch (p.tile) {
     case T256x128w8: launch_tile<T, 256, 128, 8, 4, kTileKG[0]>(A, Bt, M, N, K, p, w, epi, s); break;
@@ -726,6 +797,9 @@ int gemm_partials(const T* A, const T* Bt, int M, int N, int K, const GemmWork& 
                   hipStream_t s) {
   const GemmPlan p = plan_gemm(M, N, K, sizeof(T) == 2);
   if (p.ks <= 1) return 1;
+  if constexpr (sizeof(T) == 2) {
+    if (try_dma(A, Bt, M, N, K, p, w, EpiNone{}, s)) return p.ks;
+  }
   switch (p.tile) {
     case T256x128w8: launch_tile<T, 256, 128, 8, 4, kTileKG[0]>(A, Bt, M, N, K, p, w, EpiNone{}, s); break;
     case T128x128w8: launch_tile<T, 128, 128, 8, 4, kTileKG[1]>(A, Bt, M, N, K, p, w, EpiNone{}, s); break;
@@ -767,12 +841,23 @@ void gemm_gelu(const T* A, const T* Bt, T* out, int M, int N, int K, const GemmW
   run_gemm(A, Bt, M, N, K, w, EpiGelu<T>{out, N}, s);
 }
 
-// The large-M kernel's dynamic LDS exceeds the default limit; every
-// epilogue instantiation is raised once per device before any launch.
+// The direct-to-LDS kernels' dynamic LDS exceeds the default limit; every
+// (tile, epilogue) instance is raised once per device before any launch.
+template <class Epi>
+hipError_t allow_dma_all() {
+  hipError_t e = hipSuccess;
+#define FV_ALLOW(BM, BN, NW, WGM, NS) \
+  if (e == hipSuccess) e = allow_dma_lds<BM, BN, NW, WGM, NS, Epi>();
+  FV_DMA_TILES(FV_ALLOW)
+#undef FV_ALLOW
+  return e;
+}
+
 hipError_t gemm_prepare() {
-  const hipError_t e[] = {allow_big_lds<EpiBiasSilu<bf16_t>>(), allow_big_lds<EpiBiasF32>(),
-                          allow_big_lds<EpiQkv<bf16_t>>(),      allow_big_lds<EpiGatedResid>(),
-                          allow_big_lds<EpiGeglu<bf16_t>>(),    allow_big_lds<EpiGelu<bf16_t>>()};
+  const hipError_t e[] = {allow_dma_all<EpiBiasSilu<bf16_t>>(), allow_dma_all<EpiBiasF32>(),
+                          allow_dma_all<EpiQkv<bf16_t>>(),      allow_dma_all<EpiGatedResid>(),
+                          allow_dma_all<EpiGeglu<bf16_t>>(),    allow_dma_all<EpiGelu<bf16_t>>(),
+                          allow_dma_all<EpiNone>()};
   for (hipError_t x : e)
     if (x != hipSuccess) return x;
   return hipSuccess;
