@@ -37,6 +37,14 @@ constexpr float kHeadroom = 64.0f;  // fixed-reference headroom of the bf16 kern
 constexpr int kRG = 1;          // 16-row MFMA groups per wave
 constexpr int kRowsPerBlock = 4 * 16 * kRG;
 constexpr int kAttn16Waves = 8;  // bf16 kernel: 8 waves x 16 rows
+#ifndef FV_ATTN_STAGES
+#define FV_ATTN_STAGES 4
+#endif
+constexpr int kAttnStages = FV_ATTN_STAGES;  // K/V tile stages of the direct-load kernel
+template <int DH>
+constexpr int attn16d_lds() {
+  return kAttnStages * 2 * (32 * DH * 2);
+}
 
 template <typename T>
 constexpr int rows_per_block() {
@@ -328,6 +336,19 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 // O^T += V^T P^T with the MFMA's k index 8 g + e standing for key
 // 4 g + e (e < 4) or 16 + 4 g + e - 4 (e >= 4), and the V^T fragment reads
 // the same two 4-key runs.
+// (a plain function: the load builtin written directly in a kernel template
+// body loses the template's host-side launch stub)
+__device__ __forceinline__ void lds_dma16_attn(const void* src, void* lds) {
+  __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_attn() {  // at most N vector memory ops outstanding
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+__device__ __forceinline__ void wait_lgkmcnt0_attn() {
+  __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));
+}
+
 // (row tile, stream x kv head) of this block.  Block b runs on die b % 8 of
 // the chip (each die has its own L2); on large grids without key splits the
 // blocks of a die take a contiguous range of the (stream-major) work list,
@@ -585,6 +606,256 @@ __global__ __launch_bounds__(64 * NWV) void attn16_kernel(AttnArgs a) {
   }
 }
 
+// bf16 kernel for head dims 128 and 256 with the K and V^T tiles brought
+// straight from memory into LDS (direct-to-LDS loads, no staging registers)
+// through a ring of NS tile stages: NS - 1 tiles are in flight while one is
+// multiplied, and one barrier per tile (after which the stage of the
+// previous tile is refilled) replaces the two of the register-staged kernel.
+// Same rows, softmax, masking and output as attn16_kernel, with two layout
+// changes that the direct loads need (they write 1 KB runs of LDS, so rows
+// cannot be padded):
+//  * The score MFMA's A-operand row i of half h holds key 8 (i / 4) + 4 h +
+//    i % 4, so a lane's 8 probabilities are keys 8 lg .. 8 lg + 7 in order
+//    and its V^T operand is one 16-byte piece of a V^T row.
+//  * 16-byte piece c of K row r is stored at c ^ ((r % 4) + 4 ((r / 8) % 4))
+//    and piece c of V^T row r at c ^ ((r / 4) % 4); the 16 rows one
+//    fragment read touches then fall on 16 different bank groups.
+template <int DH, int NWV, int NS>
+__global__ __launch_bounds__(64 * NWV) void attn16d_kernel(AttnArgs a) {
+  using T = bf16_t;
+  constexpr int KT = 32;                     // keys per tile
+  constexpr int NT = 64 * NWV;               // threads
+  constexpr int RB = 16 * NWV;               // query rows per block
+  constexpr int NKS = DH / 32, NDT = DH / 16;
+  constexpr int KCH = DH / 8;                // 16-byte pieces per K row
+  constexpr int KBYTES = KT * DH * 2, VBYTES = DH * KT * 2;
+  constexpr int STAGE = KBYTES + VBYTES;
+  constexpr int NI = STAGE / 16 / NT;        // direct loads per thread per stage
+  constexpr int LDO = DH + 8;                // output staging pitch (elements)
+  static_assert(DH == 128 || DH == 256, "swizzle is laid out for 16 or 32 pieces per K row");
+  static_assert(NI * NT * 16 == STAGE && KBYTES % 1024 == 0, "stage split");
+  static_assert(NWV * 16 * LDO * 2 <= NS * STAGE, "output staging fits in the ring");
+  extern __shared__ __attribute__((aligned(16))) T attn_ring[];
+  unsigned char* ring = reinterpret_cast<unsigned char*>(attn_ring);
+
+  const int G = a.n_q_heads / a.n_kv_heads;
+  const int rows_bg = a.tokens * G;
+  int rtile, bg;
+  attn_block_of(rtile, bg);
+  const int tile0 = rtile * RB;
+  const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
+  const int split = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int P = a.len[b];
+  const int C = a.chunk_len;
+  const int l16 = lane & 15, lg = lane >> 4;
+
+  const int K = a.tokens / C;
+  const int first = K - a.n_valid[b];
+  const int rq = tile0 + 16 * wave + l16;
+  const bool valid = rq < rows_bg;
+  const int rqc = valid ? rq : rows_bg - 1;
+  const int tok = rqc / G;
+  const int head = g * G + (rqc - tok * G);
+  int klo, khi;  // this row's visible buffer keys [klo, khi); prefix keys [0, P)
+  visible_chunks(tok / C, K, first, a.mask_mode, klo, khi);
+  klo = P + C * klo;
+  khi = P + C * khi;
+  const int rlast = min(tile0 + RB - 1, rows_bg - 1);
+  const KeyTiles kts = key_tiles(P, C, K, first, a.mask_mode, tile0 / G, rlast / G, KT);
+  const int kt_begin = (split * kts.n) / a.n_split, kt_end = ((split + 1) * kts.n) / a.n_split;
+
+  bf16x8 qf[NKS];
+  {
+    const T* qrow = reinterpret_cast<const T*>(a.q) +
+                    ((size_t)(b * a.tokens + tok) * a.n_q_heads + head) * DH;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+      qf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(qrow + 32 * ks + 8 * lg));
+  }
+  f32x4 acc[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const T* kbase = reinterpret_cast<const T*>(a.karena) +
+                   ((size_t)b * a.n_kv_heads + g) * (size_t)a.S * DH;
+  const T* vbase = reinterpret_cast<const T*>(a.vtarena) +
+                   ((size_t)b * a.n_kv_heads + g) * (size_t)DH * a.S;
+  const float sl2 = 1.4426950408889634f / sqrtf((float)DH);
+
+  // The thread's piece of each of its direct loads: unit u of a stage is K
+  // (row, piece) for u < KBYTES / 16, else V^T (row, piece); offsets exclude
+  // the tile's first key.  Every load instruction is all-K or all-V^T.
+  int off[NI];
+  bool isk[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int u = 64 * (NI * wave + i) + lane;
+    isk[i] = u < KBYTES / 16;
+    if (isk[i]) {
+      const int r = u / KCH, c = (u % KCH) ^ ((r & 3) | (((r >> 3) & 3) << 2));
+      off[i] = r * DH + 8 * c;
+    } else {
+      const int v = u - KBYTES / 16;
+      const int r = v >> 2, c = (v & 3) ^ ((r >> 2) & 3);
+      off[i] = r * a.S + 8 * c;
+    }
+  }
+  auto issue = [&](int vt, int stage) __attribute__((always_inline)) {
+    const int key0 = kts.tile(vt) * KT;
+    unsigned char* st = ring + stage * STAGE + 1024 * NI * wave;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const T* src = isk[i] ? kbase + (size_t)key0 * DH + off[i] : vbase + key0 + off[i];
+      lds_dma16_attn(src, st + 1024 * i);
+    }
+  };
+  // fragment addresses within a stage
+  const int krow = 8 * (l16 >> 2) + (l16 & 3);  // K row of A-operand row l16, half 0
+  // its piece swizzle is l16 for both halves; V^T rows 16 dt + l16 share (l16 / 4) % 4
+  const int vpiece = lg ^ ((l16 >> 2) & 3);
+
+  for (int p = 0; p < NS - 1; ++p)
+    if (kt_begin + p < kt_end) issue(kt_begin + p, p);
+  // the query loads, issued before the tiles, have landed once at most the
+  // tiles' loads are outstanding (vector memory counts retire in order)
+  if (kt_end - kt_begin >= NS - 1)
+    wait_vmcnt_attn<(NS - 1) * NI>();
+  else
+    wait_vmcnt_attn<0>();
+  int kt = kt_begin, stage = 0;
+  bool staged = false;
+  float m_pending = -INFINITY;
+  while (kt < kt_end) {
+    for (; kt < kt_end; ++kt) {
+      const int key0 = kts.tile(kt) * KT;
+      if (!staged) {
+        // this wave's loads of tile kt landed (later tiles may still fly) and
+        // its reads of tile kt - 1 completed; after the barrier both hold for
+        // every wave, so tile kt - 1's stage takes tile kt + NS - 1
+        if (kt + NS - 2 < kt_end)
+          wait_vmcnt_attn<(NS - 2) * NI>();
+        else
+          wait_vmcnt_attn<0>();
+        wait_lgkmcnt0_attn();
+        __builtin_amdgcn_s_barrier();
+        if (kt + NS - 1 < kt_end) issue(kt + NS - 1, stage == 0 ? NS - 1 : stage - 1);
+      }
+      staged = false;
+      const unsigned char* sk = ring + stage * STAGE;
+      const unsigned char* sv = sk + KBYTES;
+
+      f32x4 s[2][2] = {{f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}},
+                       {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}}};
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const bf16x8 kf = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u16x8*>(sk + (krow + 4 * h) * (2 * DH) +
+                                                      16 * ((4 * ks + lg) ^ l16)));
+          s[h][ks & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], s[h][ks & 1], 0, 0, 0);
+        }
+      // sc[e]: key key0 + 8 lg + e
+      float sc[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        sc[e] = s[0][0][e] + s[0][1][e];
+        sc[4 + e] = s[1][0][e] + s[1][1][e];
+      }
+      const bool inside = key0 + KT <= P || (key0 >= klo && key0 + KT <= khi);
+      if (!__all(inside)) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int key = key0 + 8 * lg + e;
+          if (!(key < P || (key >= klo && key < khi))) sc[e] = -INFINITY;
+        }
+      }
+      float mt = sc[0];
+#pragma unroll
+      for (int e = 1; e < 8; ++e) mt = fmaxf(mt, sc[e]);
+      mt = fmaxf(mt, __shfl_xor(mt, 16));
+      mt = fmaxf(mt, __shfl_xor(mt, 32)) * sl2;
+      if (m_run == -INFINITY) m_run = mt;
+      if (__any(mt > m_run + kHeadroom)) {
+        m_pending = mt;
+        staged = true;
+        break;
+      }
+      const float m_use = m_run == -INFINITY ? 0.f : m_run;
+      float ls = 0.f;
+      u16x8 pb;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float p = exp2f(fmaf(sc[e], sl2, -m_use));
+        ls += p;
+        pb[e] = f32_to_bf16(p);
+      }
+      ls += __shfl_xor(ls, 16);
+      l_run += ls + __shfl_xor(ls, 32);
+      const bf16x8 pf = __builtin_bit_cast(bf16x8, pb);
+      // O^T (dh x queries) += V^T P^T: dh row 16 dt + l16, keys 8 lg .. 8 lg + 7
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        const bf16x8 vf = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u16x8*>(sv + (16 * dt + l16) * 64 + 16 * vpiece));
+        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, acc[dt], 0, 0, 0);
+      }
+      stage = stage + 1 == NS ? 0 : stage + 1;
+    }
+    if (staged) {
+      const float m_new = m_pending > m_run + kHeadroom ? m_pending : m_run;
+      const float alpha = m_run == -INFINITY ? 0.f : exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) acc[dt] *= alpha;
+      m_run = m_new;
+    }
+  }
+
+  // Normalised output through LDS (the ring, free once every wave is past
+  // its last tile): lane (query l16, group lg) holds dh 16 dt + 4 lg + 0..3;
+  // rows then go out whole, 16 bytes per lane.
+  const size_t R = (size_t)a.B * a.tokens * a.n_q_heads;
+  __syncthreads();
+  T* so = attn_ring + wave * 16 * LDO;
+  {
+    const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      u16x4 w;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = f32_to_bf16(acc[dt][i] * inv);
+      *reinterpret_cast<u16x4*>(so + l16 * LDO + 16 * dt + 4 * lg) = w;
+    }
+    if (a.n_split > 1 && lg == 0 && valid) {
+      const size_t grow = (size_t)(b * a.tokens + tok) * a.n_q_heads + head;
+      a.part_ml[((size_t)split * R + grow) * 2 + 0] = m_run;
+      a.part_ml[((size_t)split * R + grow) * 2 + 1] = l_run;
+    }
+  }
+  wait_lgkmcnt0_attn();  // the wave reads back only its own rows
+  {
+    constexpr int CPR = DH / 8;  // 16-byte chunks per row
+    for (int idx = lane; idx < 16 * CPR; idx += 64) {
+      const int row = idx / CPR, c = idx - row * CPR;
+      const int rq2 = tile0 + 16 * wave + row;
+      if (rq2 < rows_bg) {
+        const int tok2 = rq2 / G;
+        const int head2 = g * G + (rq2 - tok2 * G);
+        const size_t grow2 = (size_t)(b * a.tokens + tok2) * a.n_q_heads + head2;
+        T* orow = a.n_split == 1
+                      ? reinterpret_cast<T*>(a.o) + grow2 * DH
+                      : reinterpret_cast<T*>(a.part_o) + ((size_t)split * R + grow2) * DH;
+        *reinterpret_cast<u32x4*>(orow + 8 * c) =
+            *reinterpret_cast<const u32x4*>(so + row * LDO + 8 * c);
+      }
+    }
+  }
+}
+
 // Merge of split partials in split order.  Partial z holds o_z = acc_z / l_z
 // (stored in the element type) with its reference m_z and sum l_z:
 // o = sum_z 2^(m_z - M) l_z o_z / sum_z 2^(m_z - M) l_z.  One wave per row; a
@@ -646,7 +917,10 @@ void launch_dh(const AttnArgs& a, hipStream_t s, int parts) {
   constexpr int RB = rows_per_block<T>();
   dim3 grid((a.tokens * G + RB - 1) / RB, a.B * a.n_kv_heads, a.n_split);
   if (parts & 1) {
-    if constexpr (sizeof(T) == 2)
+    if constexpr (sizeof(T) == 2 && (DH == 128 || DH == 256))
+      hipLaunchKernelGGL((attn16d_kernel<DH, kAttn16Waves, kAttnStages>), grid,
+                         dim3(64 * kAttn16Waves), (attn16d_lds<DH>()), s, a);
+    else if constexpr (sizeof(T) == 2)
       hipLaunchKernelGGL((attn16_kernel<DH, kAttn16Waves>), grid, dim3(64 * kAttn16Waves), 0, s, a);
     else
       hipLaunchKernelGGL((attn_kernel<T, DH, KT, kRG>), grid, dim3(256), 0, s, a);
@@ -676,6 +950,17 @@ void launch_attention(const AttnArgs& a, hipStream_t s, int parts) {
     case 256: launch_dh<T, 256>(a, s, parts); break;
     default: break;  // rejected at fv_create
   }
+}
+
+// The direct-load kernels' dynamic LDS exceeds the default limit.
+hipError_t attention_prepare() {
+  hipError_t e = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&attn16d_kernel<128, kAttn16Waves, kAttnStages>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, attn16d_lds<128>());
+  if (e != hipSuccess) return e;
+  return hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&attn16d_kernel<256, kAttn16Waves, kAttnStages>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, attn16d_lds<256>());
 }
 
 template void launch_attention<bf16_t>(const AttnArgs&, hipStream_t, int);

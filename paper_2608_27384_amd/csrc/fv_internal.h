@@ -209,6 +209,9 @@ template <typename T>
 void launch_attention(const AttnArgs& a, hipStream_t s, int parts = 3);
 template <typename T>
 int attention_row_tiles(int tokens, int n_q_heads, int n_kv_heads);
+// Raises the dynamic LDS limit of the direct-load attention kernels (call
+// once per device before the first launch).
+hipError_t attention_prepare();
 
 // ------------------------------------------------------------------- handle
 struct GraphEntry {

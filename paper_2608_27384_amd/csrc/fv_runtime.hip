@@ -498,7 +498,10 @@ fv_status fv_create(const fv_weights* w, const fv_cfg* cfg, fv_handle* out) {
     }
 
     FV_HIP(hipGetDevice(&H.device));
-    if (H.bf16) FV_HIP(gemm_prepare());
+    if (H.bf16) {
+      FV_HIP(gemm_prepare());
+      FV_HIP(attention_prepare());
+    }
     FV_HIP(hipStreamCreateWithFlags(&H.cap_stream, hipStreamNonBlocking));
 
     // ---- weights
