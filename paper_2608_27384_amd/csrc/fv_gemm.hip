@@ -283,6 +283,15 @@ __global__ __launch_bounds__(64 * NW * KG) void gemm_kernel(const T* __restrict_
   epi.template apply<FM, FN>(acc, m0 + ar, n0 + bc, lane, M);
 }
 
+// Epilogues with an LDS-staged form (Epi::kStaged) use it in the direct-to-LDS
+// kernel, whose stage buffers are free after the main loop.
+template <class Epi, class = void>
+struct EpiStaged { static constexpr bool value = false; };
+template <class Epi>
+struct EpiStaged<Epi, std::void_t<decltype(Epi::kStaged)>> { static constexpr bool value = Epi::kStaged; };
+template <class Epi>
+constexpr bool epi_staged() { return EpiStaged<Epi>::value; }
+
 // ------------------------------------------------- direct-to-LDS bf16 GEMM
 // BM x BN output tile per block of NW waves (WGM along M).  The A and W
 // k-tiles (64 k = 128 bytes per row) go from memory straight to LDS with the
@@ -438,7 +447,13 @@ __global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(const bf16_t* __restr
       }
     return;
   }
-  epi.template apply<FM, FN>(acc, m0 + ar, n0 + bc, lane, M);
+  if constexpr (epi_staged<Epi>()) {
+    __syncthreads();  // every wave is done with the k-tile stages
+    epi.template apply_staged<FM, FN, NW, NS * STAGE>(acc, reinterpret_cast<float*>(smem), m0 + ar,
+                                                      n0 + bc, lane, wave, M);
+  } else {
+    epi.template apply<FM, FN>(acc, m0 + ar, n0 + bc, lane, M);
+  }
 }
 
 // Sum of the KS split partials of each tile, in split order, followed by the
@@ -600,7 +615,58 @@ struct EpiQkv {
 };
 
 struct EpiGatedResid {
+  static constexpr bool kStaged = true;
   float* h; const float* mod; int mod_ld, gate_off, chunk_len, ldh;
+  // Direct-to-LDS kernels: the accumulators go through the (idle) LDS so that
+  // h is read and written as whole-row 16-byte pieces, in passes of PI
+  // 32-row slabs per wave; `smem` holds NW x PI x 32 x WTN floats.
+  template <int FM, int FN, int NW, int LDS_BYTES>
+  __device__ void apply_staged(f32x16 (&acc)[FM][FN], float* smem, int row0, int col0, int lane,
+                               int wave, int M) const {
+    constexpr int WTN = 32 * FN;
+    constexpr int PI_MAX = LDS_BYTES / (NW * 32 * WTN * 4);
+    constexpr int PI = PI_MAX >= FM ? FM : (PI_MAX >= 2 && FM % 2 == 0 ? 2 : 1);
+    static_assert(PI >= 1 && FM % PI == 0, "staging does not fit");
+    constexpr int C4 = WTN / 4;                // 16-byte pieces per row
+    constexpr int PER = PI * 32 * C4 / 64;     // pieces per lane and pass
+    float* cs = smem + wave * PI * 32 * WTN;
+    float* __restrict__ hh = h;
+    const float* __restrict__ mm = mod;
+#pragma unroll
+    for (int i0 = 0; i0 < FM; i0 += PI) {
+      if (i0 > 0) __syncthreads();  // every wave done reading the last pass
+#pragma unroll
+      for (int ii = 0; ii < PI; ++ii)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            cs[(32 * ii + acc_row(r, lane)) * WTN + 32 * j + (lane & 31)] = acc[i0 + ii][j][r];
+      __syncthreads();
+#pragma unroll
+      for (int q0 = 0; q0 < PER; q0 += 8) {
+        f32x4 hv[8], gv[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {  // independent loads first
+          if (q0 + q >= PER) break;
+          const int idx = (q0 + q) * 64 + lane, rr = idx / C4, c4 = idx - rr * C4;
+          const int row = min(row0 + 32 * i0 + rr, M - 1);
+          hv[q] = *reinterpret_cast<const f32x4*>(hh + (size_t)row * ldh + col0 + 4 * c4);
+          gv[q] = *reinterpret_cast<const f32x4*>(mm + (size_t)(row / chunk_len) * mod_ld +
+                                                  gate_off + col0 + 4 * c4);
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          if (q0 + q >= PER) break;
+          const int idx = (q0 + q) * 64 + lane, rr = idx / C4, c4 = idx - rr * C4;
+          const int row = row0 + 32 * i0 + rr;
+          const f32x4 a4 = *reinterpret_cast<const f32x4*>(cs + rr * WTN + 4 * c4);
+          if (row < M)
+            *reinterpret_cast<f32x4*>(hh + (size_t)row * ldh + col0 + 4 * c4) = hv[q] + gv[q] * a4;
+        }
+      }
+    }
+  }
   template <int FM, int FN>
   __device__ void apply(f32x16 (&acc)[FM][FN], int row0, int col0, int lane, int M) const {
     float* __restrict__ hh = h;
