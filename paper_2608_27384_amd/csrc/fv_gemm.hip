@@ -305,8 +305,8 @@ constexpr bool epi_staged() { return EpiStaged<Epi>::value; }
 // k-step s.  Split-K (KS > 1) writes fp32 partials as gemm_kernel does.
 //   * 256x256, 8 waves (128x64 wave tiles), 2 stages: large M (batch 64);
 //   * 128x128, 8 waves and 64x128, 4 waves (32x64 wave tiles), 3 stages
-//     (2 on grids of several rounds): medium M (batch 1), where the deeper
-//     ring hides the load latency.
+//     (2 for 128x128 grids of several rounds): medium M (batch 1), where the
+//     deeper ring hides the load latency.
 __device__ __forceinline__ void lds_dma16(const void* src, void* lds) {
   __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
 }
@@ -761,8 +761,7 @@ void launch_tile(const T* A, const T* Bt, int M, int N, int K, const GemmPlan& p
   X(256, 256, 8, 2, 2)  \
   X(128, 128, 8, 4, 3)  \
   X(128, 128, 8, 4, 2)  \
-  X(64, 128, 4, 2, 3)   \
-  X(64, 128, 4, 2, 2)
+  X(64, 128, 4, 2, 3)
 
 template <int BM, int BN, int NW, int WGM, int NS, class Epi>
 hipError_t allow_dma_lds() {
@@ -783,10 +782,10 @@ void launch_dma(const bf16_t* A, const bf16_t* Bt, int M, int N, int K, const Ge
 }
 
 // Launches tile p.tile with the direct-to-LDS kernel when it has one;
-// returns false otherwise.  Medium tiles take three stages when the grid is
-// about one round of the chip (the deeper ring hides load latency, measured
-// 1568 against 1864 us per batch-1 step with two), two stages when it is
-// many rounds (two workgroups then fit per CU and overlap each other).
+// returns false otherwise.  The 128x128 tile takes three stages when the
+// grid is about one round of the chip (the deeper ring hides load latency,
+// measured 1568 against 1864 us per batch-1 step with two), two stages when
+// it is many rounds (two workgroups then fit per CU and overlap each other).
 template <class Epi>
 bool try_dma(const bf16_t* A, const bf16_t* Bt, int M, int N, int K, const GemmPlan& p,
              const GemmWork& w, const Epi& epi, hipStream_t s) {
@@ -799,11 +798,8 @@ bool try_dma(const bf16_t* A, const bf16_t* Bt, int M, int N, int K, const GemmP
       else
         launch_dma<128, 128, 8, 4, 3>(A, Bt, M, N, K, p, w, epi, s);
       return true;
-    case T64x128w4:
-      if (rounds)
-        launch_dma<64, 128, 4, 2, 2>(A, Bt, M, N, K, p, w, epi, s);
-      else
-        launch_dma<64, 128, 4, 2, 3>(A, Bt, M, N, K, p, w, epi, s);
+    case T64x128w4:  // chosen only below about 400 tiles x splits: one round
+      launch_dma<64, 128, 4, 2, 3>(A, Bt, M, N, K, p, w, epi, s);
       return true;
     default: return false;
   }
