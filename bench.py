@@ -190,17 +190,17 @@ def measure_streaming(w, steps, warmup, with_roofline, cached=False, mask=None):
 # Timed stages: (debug-stage id, launches per step, kernel(s) it launches).
 STAGES = {
     "film_maps": (0, "step", "gemm_kernel<..., EpiBiasF32> (all FiLM maps, one GEMM)"),
-    "qkv_gemm": (1, "layer", "gemm_kernel<..., EpiQkv> (QKV + rotary + K/V arena write)"),
-    "attention": (4, "layer", "attn16_kernel (chunk-causal + prefix attention, per-split partials)"),
+    "qkv_gemm": (1, "layer", "gemm_dma_kernel<..., EpiQkv> (QKV + rotary + K/V arena write)"),
+    "attention": (4, "layer", "attn16d_kernel (chunk-causal + prefix attention, per-split partials)"),
     "attn_combine": (5, "layer", "attn_combine (merge of the key splits)"),
-    "o_proj": (6, "layer", "split-K gemm_kernel + resid_norm_kernel (O proj, gated residual, FiLM norm)"),
-    "gate_up_gemm": (3, "layer", "gemm_kernel<..., EpiGeglu> (gate/up + GeGLU)"),
-    "down_proj": (7, "layer", "split-K gemm_kernel + resid_norm_kernel (down proj, gated residual, FiLM norm)"),
+    "o_proj": (6, "layer", "split-K gemm_dma_kernel + resid_norm_kernel (O proj, gated residual, FiLM norm)"),
+    "gate_up_gemm": (3, "layer", "gemm_dma_kernel<..., EpiGeglu> (gate/up + GeGLU)"),
+    "down_proj": (7, "layer", "split-K gemm_dma_kernel + resid_norm_kernel (down proj, gated residual, FiLM norm)"),
 }
 # stages that are one kernel launch each (eligible for the roofline record)
-SINGLE_KERNEL = {"film_maps": "gemm_kernel", "qkv_gemm": "gemm_kernel",
-                 "attention": "attn16_kernel", "attn_combine": "attn_combine",
-                 "gate_up_gemm": "gemm_kernel"}  # bf16 kernels (fp32 attention: attn_kernel)
+SINGLE_KERNEL = {"film_maps": "gemm_kernel", "qkv_gemm": "gemm_dma_kernel",
+                 "attention": "attn16d_kernel", "attn_combine": "attn_combine",
+                 "gate_up_gemm": "gemm_dma_kernel"}  # bf16 kernels (fp32 attention: attn_kernel)
 
 
 def stage_work(w, lens, n_split):

@@ -39,7 +39,7 @@ DRIVER_LAUNCHES = 20            # stage launches the driver makes
 KERNELS: Dict[str, Tuple[str, Tuple[str, ...]]] = {
     "film_maps": ("EpiBiasF32", ("csrc/fv_gemm.hip", "csrc/fv_internal.h")),
     "qkv_gemm": ("EpiQkv", ("csrc/fv_gemm.hip", "csrc/fv_internal.h")),
-    "attention": ("attn16_kernel", ("csrc/fv_attn.hip", "csrc/fv_internal.h")),
+    "attention": ("attn16d_kernel", ("csrc/fv_attn.hip", "csrc/fv_internal.h")),
     "attn_combine": ("attn_combine", ("csrc/fv_attn.hip", "csrc/fv_internal.h")),
     "gate_up_gemm": ("EpiGeglu", ("csrc/fv_gemm.hip", "csrc/fv_internal.h")),
 }
