@@ -333,6 +333,23 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 // O^T += V^T P^T with the MFMA's k index 8 g + e standing for key
 // 4 g + e (e < 4) or 16 + 4 g + e - 4 (e >= 4), and the V^T fragment reads
 // the same two 4-key runs.
+// Reductions over the lanes l, l ^ 16, l ^ 32, l ^ 48 of a wave with the
+// gfx950 lane swaps (VALU, no LDS): swapping a value with itself across
+// 16-lane rows (32-lane halves) hands each lane the pair {x[l], x[l ^ 16]}
+// ({x[l], x[l ^ 32]}) in its two results.
+__device__ __forceinline__ float max_xor16_32(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float sum_xor16_32(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // (a plain function: the load builtin written directly in a kernel template
 // body loses the template's host-side launch stub)
 __device__ __forceinline__ void lds_dma16_attn(const void* src, void* lds) {
@@ -521,8 +538,7 @@ __global__ __launch_bounds__(64 * NWV) void attn16_kernel(AttnArgs a) {
       float mt = sc[0];
 #pragma unroll
       for (int e = 1; e < 8; ++e) mt = fmaxf(mt, sc[e]);
-      mt = fmaxf(mt, __shfl_xor(mt, 16));
-      mt = fmaxf(mt, __shfl_xor(mt, 32)) * sl2;
+      mt = max_xor16_32(mt) * sl2;
       if (m_run == -INFINITY) m_run = mt;
       if (__any(mt > m_run + kHeadroom)) {
         m_pending = mt;
@@ -538,8 +554,7 @@ __global__ __launch_bounds__(64 * NWV) void attn16_kernel(AttnArgs a) {
         ls += p;
         pb[e] = f32_to_bf16(p);
       }
-      ls += __shfl_xor(ls, 16);
-      l_run += ls + __shfl_xor(ls, 32);
+      l_run += sum_xor16_32(ls);
       const bf16x8 pf = __builtin_bit_cast(bf16x8, pb);
       // O^T (dh x queries) += V^T P^T: dh row 16 dt + l16, keys 4 lg + 0..3
       // and 16 + 4 lg + 0..3
@@ -773,8 +788,7 @@ __global__ __launch_bounds__(64 * NWV) void attn16d_kernel(AttnArgs a) {
       float mt = sc[0];
 #pragma unroll
       for (int e = 1; e < 8; ++e) mt = fmaxf(mt, sc[e]);
-      mt = fmaxf(mt, __shfl_xor(mt, 16));
-      mt = fmaxf(mt, __shfl_xor(mt, 32)) * sl2;
+      mt = max_xor16_32(mt) * sl2;
       if (m_run == -INFINITY) m_run = mt;
       if (__any(mt > m_run + kHeadroom)) {
         m_pending = mt;
@@ -790,8 +804,7 @@ __global__ __launch_bounds__(64 * NWV) void attn16d_kernel(AttnArgs a) {
         ls += p;
         pb[e] = f32_to_bf16(p);
       }
-      ls += __shfl_xor(ls, 16);
-      l_run += ls + __shfl_xor(ls, 32);
+      l_run += sum_xor16_32(ls);
       const bf16x8 pf = __builtin_bit_cast(bf16x8, pb);
       // O^T (dh x queries) += V^T P^T: dh row 16 dt + l16, keys 8 lg .. 8 lg + 7
 #pragma unroll
