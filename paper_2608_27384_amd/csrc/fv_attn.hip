@@ -885,15 +885,14 @@ __global__ __launch_bounds__(256) void attn_combine(const T* __restrict__ part_o
     lz[z] = z < n_split ? part_ml[((size_t)z * R + row) * 2 + 1] : 0.f;
   }
   constexpr int NV = (DH + 255) / 256;  // 4-feature groups per lane
-  float pv[8][NV][4];
+  f32x4 pv[8][NV];
 #pragma unroll
   for (int z = 0; z < 8; ++z)
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int d = 4 * lane + 256 * v;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        pv[z][v][i] = (z < n_split && d < DH) ? to_f32(part_o[((size_t)z * R + row) * DH + d + i]) : 0.f;
+      pv[z][v] = (z < n_split && d < DH) ? load4_f32(part_o + ((size_t)z * R + row) * DH + d)
+                                         : f32x4{0.f, 0.f, 0.f, 0.f};
     }
   float M = -INFINITY;
 #pragma unroll
@@ -909,13 +908,10 @@ __global__ __launch_bounds__(256) void attn_combine(const T* __restrict__ part_o
   for (int v = 0; v < NV; ++v) {
     const int d = 4 * lane + 256 * v;
     if (d >= DH) continue;
+    f32x4 num = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float num = 0.f;
-#pragma unroll
-      for (int z = 0; z < 8; ++z) num += mz[z] * pv[z][v][i];
-      o[(size_t)row * DH + d + i] = from_f32<T>(num * inv);
-    }
+    for (int z = 0; z < 8; ++z) num += mz[z] * pv[z][v];
+    store4<T>(o + (size_t)row * DH + d, num[0] * inv, num[1] * inv, num[2] * inv, num[3] * inv);
   }
 }
 

@@ -62,6 +62,12 @@ template <> struct Mfma<float> {
   }
 };
 
+// Four consecutive elements as fp32 (16-byte fp32 or 8-byte bf16 load; p aligned to that).
+__device__ __forceinline__ f32x4 load4_f32(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+__device__ __forceinline__ f32x4 load4_f32(const bf16_t* p) {
+  const u16x4 v = *reinterpret_cast<const u16x4*>(p);
+  return f32x4{to_f32(v[0]), to_f32(v[1]), to_f32(v[2]), to_f32(v[3])};
+}
 // Four consecutive elements (16-byte fp32 or 8-byte bf16 store; p aligned to that).
 template <typename T>
 __device__ __forceinline__ void store4(T* p, float a, float b, float c, float d);

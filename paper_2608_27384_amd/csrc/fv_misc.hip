@@ -264,13 +264,21 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const float* __restrict
     }
   }
   if (norm_off < 0) return;
+  f32x4 svq[2], bvq[2];  // the norm's maps are requested before the row sum waits
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int c = 4 * tid + 1024 * q;
+    if (c < W) {
+      svq[q] = *reinterpret_cast<const f32x4*>(mrow + norm_off + c);
+      bvq[q] = *reinterpret_cast<const f32x4*>(mrow + norm_off + W + c);
+    }
+  }
   const float rinv = 1.0f / sqrtf(block_sum_256(ss, red) / (float)W + eps);
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const int c = 4 * tid + 1024 * q;
     if (c < W) {
-      const f32x4 sv = *reinterpret_cast<const f32x4*>(mrow + norm_off + c);
-      const f32x4 bv = *reinterpret_cast<const f32x4*>(mrow + norm_off + W + c);
+      const f32x4 sv = svq[q], bv = bvq[q];
       const f32x4 hv = hq[q];
       store4<T>(u + (size_t)row * W + c, hv[0] * rinv * (1.0f + sv[0]) + bv[0],
                 hv[1] * rinv * (1.0f + sv[1]) + bv[1], hv[2] * rinv * (1.0f + sv[2]) + bv[2],
