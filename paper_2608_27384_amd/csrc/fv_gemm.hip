@@ -733,6 +733,51 @@ struct EpiGelu {
   }
 };
 
+// ------------------------------------------------------ few-row GEMM (GEMV)
+// out[m][n] = silu(sum_k A[m][k] W[n][k] + bias[n]) for M <= kGemvRows rows
+// (the time-MLP at small batch): one wave per output column n, lanes take
+// 16-byte pieces of k (the weight row once, every input row at the same
+// pieces), fp32 sums reduced across the wave.  One launch, no split-K pass.
+constexpr int kGemvRows = 16;
+template <typename T>
+__global__ __launch_bounds__(256) void gemv_bias_silu_kernel(const T* __restrict__ A,
+                                                             const T* __restrict__ Bt,
+                                                             const float* __restrict__ bias,
+                                                             T* __restrict__ out, int M, int N,
+                                                             int K) {
+  constexpr int EPV = 16 / (int)sizeof(T);  // elements per 16-byte piece
+  const int lane = threadIdx.x & 63;
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  float acc[kGemvRows];
+#pragma unroll
+  for (int m = 0; m < kGemvRows; ++m) acc[m] = 0.f;
+  const T* wrow = Bt + (size_t)n * K;
+  for (int k0 = EPV * lane; k0 < K; k0 += 64 * EPV) {
+    float wv[EPV];
+    {
+      const u32x4 raw = *reinterpret_cast<const u32x4*>(wrow + k0);
+      const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+      for (int i = 0; i < EPV; ++i) wv[i] = to_f32(e[i]);
+    }
+#pragma unroll
+    for (int m = 0; m < kGemvRows; ++m) {
+      if (m >= M) break;
+      const u32x4 raw = *reinterpret_cast<const u32x4*>(A + (size_t)m * K + k0);
+      const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+      for (int i = 0; i < EPV; ++i) acc[m] = fmaf(to_f32(e[i]), wv[i], acc[m]);
+    }
+  }
+  const float b = bias[n];
+#pragma unroll
+  for (int m = 0; m < kGemvRows; ++m) {
+    if (m >= M) break;
+    const float v = wave_sum(acc[m]);
+    if (lane == 0) out[(size_t)m * N + n] = from_f32<T>(silu_f(v + b));
+  }
+}
+
 // -------------------------------------------------------------- tile choice
 // Tile shapes (BM x BN, waves); every wave owns a sub-tile at least 64
 // columns wide, so paired epilogues find both partners of a 64-column pair
@@ -874,6 +919,11 @@ int gemm_partials(const T* A, const T* Bt, int M, int N, int K, const GemmWork& 
 template <typename T>
 void gemm_bias_silu(const T* A, const T* Bt, const float* bias, T* out, int M, int N, int K,
                     const GemmWork& w, hipStream_t s) {
+  if (M <= kGemvRows && N % 4 == 0 && K % (16 / (int)sizeof(T)) == 0) {
+    hipLaunchKernelGGL((gemv_bias_silu_kernel<T>), dim3(N / 4), dim3(256), 0, s, A, Bt, bias, out,
+                       M, N, K);
+    return;
+  }
   run_gemm(A, Bt, M, N, K, w, EpiBiasSilu<T>{out, bias, N}, s);
 }
 template <typename T>

@@ -10,26 +10,6 @@ namespace {
 constexpr double kTwoPi = 6.283185307179586476925286766559;
 
 // ------------------------------------------------------------------ helpers
-// Sum over the 64 lanes, the same value in every lane, without LDS
-// permutes: the gfx950 lane swaps exchange across 32-lane halves and 16-lane
-// rows; DPP row rotations by 8 and 4 and quad permutes (xor 2, xor 1) finish
-// within a row.  Every lane adds the same pairs, so all lanes agree bit for
-// bit.
-template <int CTRL>
-__device__ __forceinline__ float dpp_add(float x) {
-  return x + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
-}
-__device__ __forceinline__ float wave_sum(float x) {
-  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = __uint_as_float(b[0]) + __uint_as_float(b[1]);
-  x = dpp_add<0x128>(x);  // row_ror:8
-  x = dpp_add<0x124>(x);  // row_ror:4
-  x = dpp_add<0x4E>(x);   // quad_perm [2,3,0,1]
-  x = dpp_add<0xB1>(x);   // quad_perm [1,0,3,2]
-  return x;
-}
 
 // -------------------------------------------------------- time embedding
 // e[row] = [sin(2 pi t / p_i) | cos(2 pi t / p_i)], p_i = 4e-3 * (4/4e-3)^(i/(W/2-1)),
