@@ -92,8 +92,8 @@ class Inputs:
         else:
             self.kd, self.vd = torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda()
         self.host_k, self.host_v = k, v
-        self.x = synth.make_buffer(w, seed)
-        self.t = synth.noise_levels_batched(w)
+        self.x = np.array(synth.make_buffer(w, seed))  # writable copies for torch
+        self.t = np.array(synth.noise_levels_batched(w))
 
 
 def _events(n):

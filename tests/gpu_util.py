@@ -24,7 +24,7 @@ def dev_prefix(w, k, v):
 
 def dev(x):
     torch = torch_mod()
-    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()
+    return torch.from_numpy(np.array(x, dtype=np.float32)).cuda()  # a writable copy
 
 
 def host(t):
