@@ -14,8 +14,11 @@
 // pairs of its query-head group, flattened token-major; a block takes
 // consecutive rows, 16 per wave (bf16: 8 waves, 128 rows; fp32: 4 waves, 64
 // rows, RG groups of 16 rows per wave sharing every K and V fragment read
-// from LDS), so rows of all heads that share the kv head reuse one K/V tile.  The next K/V tile is loaded into registers
-// while the current one is multiplied.  Rows of a block may straddle a chunk
+// from LDS), so rows of all heads that share the kv head reuse one K/V tile.
+// For bf16 head dims 128 and 256 (attn16d_kernel) the K/V tiles go from
+// memory straight into a ring of LDS stages, three tiles ahead; otherwise the
+// next K/V tile is loaded into registers while the current one is
+// multiplied.  Rows of a block may straddle a chunk
 // boundary; each lane masks with its own row's limit.  Optionally the key
 // tiles of a block are split over gridDim.z blocks whose normalised partial
 // outputs (in the element type) and (max, sum) are merged in a fixed order

@@ -4,8 +4,14 @@
 // projection, packed gate/up, down projection) is C = A * W with A the
 // activations [M][K] (row-major) and W stored output-major as Bt [N][K].
 //
-// Block: NW waves (2, 4 or 8).  Tile BM x BN; k is staged through LDS 128
-// bytes per row (64 bf16 / 32 fp32) at a time in two buffers.  While a wave
+// Two main loops.  The bf16 tiles 256x256, 128x128 and 64x128 use
+// gemm_dma_kernel: k-tiles go from memory straight into a ring of LDS stages
+// with the direct-to-LDS loads (see there).  The fp32 tiles and the small-M
+// 32x128 tile use gemm_kernel, described here, and M <= 16 time-MLP layers a
+// GEMV.
+//
+// gemm_kernel block: NW waves (2, 4 or 8).  Tile BM x BN; k is staged through
+// LDS 128 bytes per row (64 bf16 / 32 fp32) at a time in two buffers.  While a wave
 // multiplies the tile in one buffer with 32x32 MFMA instructions, the
 // registers holding the next tile are written to the other buffer piece by
 // piece between k-steps, and every freed register piece immediately issues
