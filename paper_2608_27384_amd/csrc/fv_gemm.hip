@@ -36,6 +36,9 @@
 //    len[b] + token, so attention reads [prefix ; buffer] as one key range;
 //  * gated residual h += gate[chunk] * acc;
 //  * GeGLU gelu(g) * u and plain GELU.
+// Element-type outputs of the QKV and GELU epilogues are transposed within
+// each group of four lanes first, so a lane stores four consecutive columns
+// of one row at once.
 // Paired epilogues rely on the weight packing: columns [64p, 64p+32) and
 // [64p+32, 64p+64) of a packed matrix hold the two partners of a pair, which
 // then sit in the same lane and register of two adjacent 32-column tiles.
@@ -72,6 +75,40 @@ template <> struct Mf32<float> {
 
 __device__ __forceinline__ int acc_row(int r, int lane) {
   return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+}
+
+// Registers 4q .. 4q+3 of a 32x32 accumulator hold four consecutive rows of
+// the lane's column.  quad_rows transposes each such 4x4 block within its
+// group of four lanes: lane l gets back row 8q + 4 (l / 32) + (l & 3) at the
+// columns (l & 28) .. (l & 28) + 3 of the 32-column block, so a row's four
+// outputs leave as one store instead of four 2-byte ones.  Every lane of the
+// wave must be active.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ f32x4 quad_rows(float x0, float x1, float x2, float x3, int lane) {
+  const bool b0 = lane & 1, b1 = lane & 2;
+  // lanes l, l^1 trade: each then holds two adjacent columns of the rows
+  // (l & 1) and 2 + (l & 1)
+  const float r1 = dpp_mov<0xB1>(b0 ? x0 : x1);  // quad_perm [1,0,3,2]
+  const float r2 = dpp_mov<0xB1>(b0 ? x2 : x3);
+  const float z0 = b0 ? r1 : x0, z1 = b0 ? x1 : r1;
+  const float z2 = b0 ? r2 : x2, z3 = b0 ? x3 : r2;
+  // lanes l, l^2 trade column pairs
+  const float t1 = dpp_mov<0x4E>(b1 ? z0 : z2);  // quad_perm [2,3,0,1]
+  const float t2 = dpp_mov<0x4E>(b1 ? z1 : z3);
+  return b1 ? f32x4{t1, t2, z2, z3} : f32x4{z0, z1, t1, t2};
+}
+// store of the four transposed values at p (4-element aligned when `vec`)
+template <typename T>
+__device__ __forceinline__ void store_quad(T* p, const f32x4& u, bool vec) {
+  if (vec) {
+    store4<T>(p, u[0], u[1], u[2], u[3]);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) p[e] = from_f32<T>(u[e]);
+  }
 }
 
 // Output tile of this block.  Block b of a launch runs on XCD b % 8 (the
@@ -307,8 +344,11 @@ constexpr bool epi_staged() { return EpiStaged<Epi>::value; }
 // without padding.  One barrier per k-tile, after every wave's last fragment
 // reads of the tile; the loads of tile k + NS are issued right after it into
 // the stage just consumed, so NS - 1 tiles are in flight while one is
-// multiplied.  Fragments of k-step s + 1 are read during the MFMAs of
-// k-step s.  Split-K (KS > 1) writes fp32 partials as gemm_kernel does.
+// multiplied.  Fragments of k-step s + LA are read during the MFMAs of
+// k-step s (LA = 2 for the 32x64 wave tiles, 1 for 128x64), so the barrier
+// comes LA - 1 k-steps before the end of a tile, once the wave has issued
+// its last read of it.  Split-K (KS > 1) writes fp32 partials as gemm_kernel
+// does.
 //   * 256x256, 8 waves (128x64 wave tiles), 2 stages: large M (batch 64);
 //   * 128x128, 8 waves and 64x128, 4 waves (32x64 wave tiles), 3 stages
 //     (2 for 128x128 grids of several rounds): medium M (batch 1), where the
@@ -336,6 +376,10 @@ __global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(const bf16_t* __restr
                                                            float* __restrict__ ws, Epi epi) {
   constexpr int WGN = NW / WGM, WTM = BM / WGM, WTN = BN / WGN, FM = WTM / 32, FN = WTN / 32;
   constexpr int BK = 64, NSTEP = 4;
+  // k-steps whose fragments are read ahead: two for the 32x64 wave tiles,
+  // whose two MFMAs per k-step are shorter than an LDS read (QKV at batch 1
+  // 10.4 -> 10.2 us); one where a k-step has 8 MFMAs
+  constexpr int LA = FM * FN >= 4 ? 1 : 2;
   constexpr int STAGE = (BM + BN) * 128;        // bytes
   constexpr int NI = (BM + BN) * 8 / (64 * NW);  // direct loads per wave per stage
   static_assert(NI * 64 * NW == (BM + BN) * 8 && FM >= 1 && FN >= 1 && NS >= 2, "bad tile");
@@ -375,7 +419,10 @@ __global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(const bf16_t* __restr
   const int lr = lane & 31, lg = lane >> 5;
   const int swz = (lr >> 1) & 7;  // rows 32 i + lr of any fragment share it
   const int arow = wm * WTM, brow = BM + wn * WTN;
-  u32x4 af[2][FM], bfr[2][FN];
+  // fragment slots: the k-step index within the tile when reading LA > 1
+  // steps ahead, else alternate
+  constexpr int NSL = LA == 1 ? 2 : NSTEP;
+  u32x4 af[NSL][FM], bfr[NSL][FN];
   auto read_frags = [&](int slot, int stage, int ks) __attribute__((always_inline)) {
     const bf16_t* st = reinterpret_cast<const bf16_t*>(smem + stage * STAGE);
     const int co = 8 * ((2 * ks + lg) ^ swz);
@@ -395,27 +442,32 @@ __global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(const bf16_t* __restr
   else
     wait_vmcnt<0>();
   __builtin_amdgcn_s_barrier();
-  read_frags(0, 0, 0);
+#pragma unroll
+  for (int p = 0; p < LA; ++p) read_frags(p % NSL, 0, p);
   int stage = 0;
   for (int kt = kt0; kt < kt1; ++kt) {
     const int nstage = stage + 1 == NS ? 0 : stage + 1;
 #pragma unroll
     for (int ks = 0; ks < NSTEP; ++ks) {
-      const int cb = ks & 1;
-      if (ks + 1 < NSTEP) {
-        read_frags(cb ^ 1, stage, ks + 1);
+      const int cb = ks % NSL;
+      const int rs = ks + LA;  // k-step read now (rs >= NSTEP: of tile kt + 1)
+      if (rs < NSTEP) {
+        read_frags(rs % NSL, stage, rs);
       } else {
-        // this wave's loads of tile kt + 1 landed (later ones may still fly)
-        // and its reads of tile kt completed; after the barrier both hold for
-        // every wave, and this stage is free for tile kt + NS
-        if (kt + NS - 1 < kt1)
-          wait_vmcnt<(NS - 2) * NI>();
-        else
-          wait_vmcnt<0>();
-        wait_lgkmcnt0();
-        __builtin_amdgcn_s_barrier();
-        if (kt + NS < kt1) issue(kt + NS, stage);
-        if (kt + 1 < kt1) read_frags(cb ^ 1, nstage, 0);
+        if (rs == NSTEP) {
+          // this wave's loads of tile kt + 1 landed (later ones may still
+          // fly) and its reads of tile kt, all issued by now, completed; after
+          // the barrier both hold for every wave, and this stage is free for
+          // tile kt + NS
+          if (kt + NS - 1 < kt1)
+            wait_vmcnt<(NS - 2) * NI>();
+          else
+            wait_vmcnt<0>();
+          wait_lgkmcnt0();
+          __builtin_amdgcn_s_barrier();
+          if (kt + NS < kt1) issue(kt + NS, stage);
+        }
+        if (kt + 1 < kt1) read_frags(rs % NSL, nstage, rs - NSTEP);
       }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
@@ -424,7 +476,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(const bf16_t* __restr
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
               __builtin_bit_cast(bf16x8, af[cb][i]), __builtin_bit_cast(bf16x8, bfr[cb][j]),
               acc[i][j], 0, 0, 0);
-      if (ks + 1 < NSTEP) {  // one fragment read after each MFMA
+      if (rs != NSTEP) {  // one fragment read after each MFMA
         constexpr int nrd = FM + FN < FM * FN ? FM + FN : FM * FN;
 #pragma unroll
         for (int q = 0; q < nrd; ++q) {
@@ -568,23 +620,40 @@ struct EpiQkv {
           const bool isq = c0 < qd;
           const int cc = isq ? c0 : c0 - qd;
           const int head = cc / dh;
-          const int dlo = 32 * ((cc - head * dh) >> 6) + (lane & 31), dhi = dlo + half;
+          const int dlo = 32 * ((cc - head * dh) >> 6) + (lane & 31);
           float cs[16], sn[16];
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             cs[r] = rcos[(size_t)rp[r].y * half + dlo];
             sn[r] = rsin[(size_t)rp[r].y * half + dlo];
           }
+          // rotated pair (d, d + dh/2) per register, then each group of
+          // four rows transposed so a lane writes 4 features of one row
+          const int d0 = dlo & ~3, k4 = lane & 3;
+          // (stream, position) of the row each lane writes (K rows only)
+          int2 pw[4];
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int row = row0 + 32 * i + acc_row(r, lane);
+          for (int q4 = 0; q4 < 4; ++q4)
+            pw[q4] = isq ? int2{0, 0}
+                         : row_pos[min(row0 + 32 * i + 8 * q4 + 4 * (lane >> 5) + k4, M - 1)];
+#pragma unroll
+          for (int q4 = 0; q4 < 4; ++q4) {
+            float y0[4], y1[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int r = 4 * q4 + e;
+              const float x0 = acc[i][j][r], x1 = acc[i][j + 1][r];
+              y0[e] = x0 * cs[r] - x1 * sn[r];
+              y1[e] = x1 * cs[r] + x0 * sn[r];
+            }
+            const f32x4 u0 = quad_rows(y0[0], y0[1], y0[2], y0[3], lane);
+            const f32x4 u1 = quad_rows(y1[0], y1[1], y1[2], y1[3], lane);
+            const int row = row0 + 32 * i + 8 * q4 + 4 * (lane >> 5) + k4;
             if (row >= M) continue;
-            const float x0 = acc[i][j][r], x1 = acc[i][j + 1][r];
-            const float y0 = x0 * cs[r] - x1 * sn[r], y1 = x1 * cs[r] + x0 * sn[r];
             T* dst = isq ? a.q + (size_t)row * qd + head * dh
-                         : a.karena + (((size_t)rp[r].x * a.n_kv_heads + head) * a.S + rp[r].y) * dh;
-            dst[dlo] = from_f32<T>(y0);
-            dst[dhi] = from_f32<T>(y1);
+                         : a.karena + (((size_t)pw[q4].x * a.n_kv_heads + head) * a.S + pw[q4].y) * dh;
+            store4<T>(dst + d0, u0[0], u0[1], u0[2], u0[3]);
+            store4<T>(dst + d0 + half, u1[0], u1[1], u1[2], u1[3]);
           }
         } else {
           // V^T rows: registers 4q..4q+3 of a lane are 4 consecutive tokens,
@@ -704,17 +773,21 @@ struct EpiGeglu {
   template <int FM, int FN>
   __device__ void apply(f32x16 (&acc)[FM][FN], int row0, int col0, int lane, int M) const {
     static_assert(FN % 2 == 0, "GeGLU epilogue needs column pairs");
+    const bool vec = (ldo & 3) == 0;
 #pragma unroll
     for (int j = 0; j < FN; j += 2) {
-      const int col = ((col0 + 32 * j) >> 1) + (lane & 31);
+      const int col = ((col0 + 32 * j) >> 1) + (lane & 28);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = row0 + 32 * i + acc_row(r, lane);
-          if (row < M)
-            out[(size_t)row * ldo + col] =
-                from_f32<T>(gelu_tanh_f(acc[i][j][r]) * acc[i][j + 1][r]);
+        for (int q4 = 0; q4 < 4; ++q4) {
+          float y[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            y[e] = gelu_tanh_f(acc[i][j][4 * q4 + e]) * acc[i][j + 1][4 * q4 + e];
+          const f32x4 u = quad_rows(y[0], y[1], y[2], y[3], lane);
+          const int row = row0 + 32 * i + 8 * q4 + 4 * (lane >> 5) + (lane & 3);
+          if (row < M) store_quad<T>(out + (size_t)row * ldo + col, u, vec);
         }
     }
   }
@@ -725,15 +798,20 @@ struct EpiGelu {
   T* out; int ldo;
   template <int FM, int FN>
   __device__ void apply(f32x16 (&acc)[FM][FN], int row0, int col0, int lane, int M) const {
+    const bool vec = (ldo & 3) == 0;
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
-      const int col = col0 + 32 * j + (lane & 31);
+      const int col = col0 + 32 * j + (lane & 28);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = row0 + 32 * i + acc_row(r, lane);
-          if (row < M) out[(size_t)row * ldo + col] = from_f32<T>(gelu_tanh_f(acc[i][j][r]));
+        for (int q4 = 0; q4 < 4; ++q4) {
+          float y[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) y[e] = gelu_tanh_f(acc[i][j][4 * q4 + e]);
+          const f32x4 u = quad_rows(y[0], y[1], y[2], y[3], lane);
+          const int row = row0 + 32 * i + 8 * q4 + 4 * (lane >> 5) + (lane & 3);
+          if (row < M) store_quad<T>(out + (size_t)row * ldo + col, u, vec);
         }
     }
   }
