@@ -642,6 +642,8 @@ __global__ __launch_bounds__(64 * NWV) void attn16d_kernel(AttnArgs a) {
   constexpr int NT = 64 * NWV;               // threads
   constexpr int RB = 16 * NWV;               // query rows per block
   constexpr int NKS = DH / 32, NDT = DH / 16;
+  constexpr int NKF = 2 * NKS;               // K fragments per tile
+  constexpr int DK = NKF < 8 ? NKF : 8, DV = NDT < 8 ? NDT : 8;  // read-ahead depths
   constexpr int KCH = DH / 8;                // 16-byte pieces per K row
   constexpr int KBYTES = KT * DH * 2, VBYTES = DH * KT * 2;
   constexpr int STAGE = KBYTES + VBYTES;
@@ -762,17 +764,43 @@ __global__ __launch_bounds__(64 * NWV) void attn16d_kernel(AttnArgs a) {
       const unsigned char* sk = ring + stage * STAGE;
       const unsigned char* sv = sk + KBYTES;
 
+      // K fragment idx = 2 ks + h and V^T fragment dt are read DK / DV ahead
+      // of their MFMA from register rings; the first V^T reads are issued
+      // before the softmax arithmetic, which hides their latency
+      auto kread = [&](int idx) __attribute__((always_inline)) {
+        return __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u16x8*>(sk + (krow + 4 * (idx & 1)) * (2 * DH) +
+                                                    16 * ((4 * (idx >> 1) + lg) ^ l16)));
+      };
+      auto vread = [&](int dt) __attribute__((always_inline)) {
+        return __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u16x8*>(sv + (16 * dt + l16) * 64 + 16 * vpiece));
+      };
+      bf16x8 kf[DK];
+#pragma unroll
+      for (int i = 0; i < DK; ++i) kf[i] = kread(i);
       f32x4 s[2][2] = {{f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}},
                        {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}}};
 #pragma unroll
-      for (int ks = 0; ks < NKS; ++ks)
+      for (int idx = 0; idx < NKF; ++idx) {
+        const int ks = idx >> 1, h = idx & 1;
+        s[h][ks & 1] =
+            __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[idx % DK], qf[ks], s[h][ks & 1], 0, 0, 0);
+        if (idx + DK < NKF) kf[idx % DK] = kread(idx + DK);
+      }
+      bf16x8 vf[DV];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const bf16x8 kf = __builtin_bit_cast(
-              bf16x8, *reinterpret_cast<const u16x8*>(sk + (krow + 4 * h) * (2 * DH) +
-                                                      16 * ((4 * ks + lg) ^ l16)));
-          s[h][ks & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], s[h][ks & 1], 0, 0, 0);
-        }
+      for (int i = 0; i < DV; ++i) vf[i] = vread(i);
+      // issue order: DK reads, then one read (K, then the first V^T) after
+      // each score MFMA
+      static_assert(NKF - DK + DV == NKF, "one read per score MFMA");
+      __builtin_amdgcn_sched_group_barrier(0x100, DK, 0);
+#pragma unroll
+      for (int i = 0; i < NKF; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
       // sc[e]: key key0 + 8 lg + e
       float sc[8];
 #pragma unroll
@@ -803,7 +831,9 @@ __global__ __launch_bounds__(64 * NWV) void attn16d_kernel(AttnArgs a) {
       u16x8 pb;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float p = exp2f(fmaf(sc[e], sl2, -m_use));
+        // raw hardware exp2: a probability below 2^-126 (flushed to 0) is
+        // negligible against the row's sum
+        const float p = __builtin_amdgcn_exp2f(fmaf(sc[e], sl2, -m_use));
         ls += p;
         pb[e] = f32_to_bf16(p);
       }
@@ -812,9 +842,8 @@ __global__ __launch_bounds__(64 * NWV) void attn16d_kernel(AttnArgs a) {
       // O^T (dh x queries) += V^T P^T: dh row 16 dt + l16, keys 8 lg .. 8 lg + 7
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
-        const bf16x8 vf = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u16x8*>(sv + (16 * dt + l16) * 64 + 16 * vpiece));
-        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, acc[dt], 0, 0, 0);
+        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt % DV], pf, acc[dt], 0, 0, 0);
+        if (dt + DV < NDT) vf[dt % DV] = vread(dt + DV);
       }
       stage = stage + 1 == NS ? 0 : stage + 1;
     }
