@@ -553,7 +553,7 @@ __global__ __launch_bounds__(64 * NWV) void attn16_kernel(AttnArgs a) {
       u16x8 pb;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float p = exp2f(fmaf(sc[e], sl2, -m_use));
+        const float p = __builtin_amdgcn_exp2f(fmaf(sc[e], sl2, -m_use));  // see attn16d_kernel
         ls += p;
         pb[e] = f32_to_bf16(p);
       }

@@ -101,15 +101,19 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
-// Both activations are evaluated as x / (1 + 2^a) with the hardware exp2
-// and reciprocal (a few instructions instead of the library tanh); the
-// tanh-form GELU uses 0.5 (1 + tanh(u)) = 1 / (1 + exp(-2u)).
+// Both activations are evaluated as x / (1 + 2^a) with the bare hardware
+// exp2 and reciprocal instructions (1 ulp each; a few instructions instead
+// of the library tanh, and instead of the range handling of exp2f and the
+// IEEE division sequence); the tanh-form GELU uses
+// 0.5 (1 + tanh(u)) = 1 / (1 + exp(-2u)).  The limits hold: 2^a = inf gives
+// 0, and 2^a below the normal range (flushed to 0) gives x.
 __device__ __forceinline__ float silu_f(float x) {
-  return __fdividef(x, 1.0f + exp2f(-1.4426950408889634f * x));
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * x));
 }
 __device__ __forceinline__ float gelu_tanh_f(float x) {
   const float c = -2.0f * 0.7978845608028654f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
-  return __fdividef(x, 1.0f + exp2f(c * fmaf(0.044715f * x, x * x, x)));
+  return x * __builtin_amdgcn_rcpf(
+                 1.0f + __builtin_amdgcn_exp2f(c * fmaf(0.044715f * x, x * x, x)));
 }
 
 // ------------------------------------------------------------ GEMM launches
