@@ -604,15 +604,31 @@ struct EpiQkv {
     static_assert(FN % 2 == 0, "QKV epilogue needs column pairs");
     const int dh = a.head_dim, half = dh / 2;
     const int qd = a.n_q_heads * dh, kd = a.n_kv_heads * dh;
-    const int2* __restrict__ row_pos = a.row_pos;
     const float* __restrict__ rcos = a.rcos;
     const float* __restrict__ rsin = a.rsin;
+    // (stream, arena row) of a token row: b = row / tokens, len[b] + row -
+    // b tokens.  The wave's rows span at most two streams when tokens >= 32
+    // FM: their two lengths are read once (no per-row lookup ahead of the
+    // rotary tables); otherwise every row looks its stream up.
+    const int ntok = a.tokens;
+    const int b_lo = min(row0, M - 1) / ntok, b_hi = min(row0 + 32 * FM - 1, M - 1) / ntok;
+    const bool two = b_hi - b_lo <= 1;
+    const int len_lo = a.len[b_lo], len_hi = a.len[b_hi], row_hi = b_hi * ntok;
+    auto locate = [&](int row) __attribute__((always_inline)) {
+      row = min(row, M - 1);
+      if (two) {
+        const bool hi = row >= row_hi;
+        const int b = hi ? b_hi : b_lo;
+        return int2{b, (hi ? len_hi : len_lo) + row - b * ntok};
+      }
+      const int b = row / ntok;
+      return int2{b, a.len[b] + row - b * ntok};
+    };
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
-      // all row lookups of this 32-row slab first (they are independent)
       int2 rp[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) rp[r] = row_pos[min(row0 + 32 * i + acc_row(r, lane), M - 1)];
+      for (int r = 0; r < 16; ++r) rp[r] = locate(row0 + 32 * i + acc_row(r, lane));
 #pragma unroll
       for (int j = 0; j < FN; j += 2) {
         const int c0 = col0 + 32 * j;  // first packed column of the pair group
@@ -634,8 +650,7 @@ struct EpiQkv {
           int2 pw[4];
 #pragma unroll
           for (int q4 = 0; q4 < 4; ++q4)
-            pw[q4] = isq ? int2{0, 0}
-                         : row_pos[min(row0 + 32 * i + 8 * q4 + 4 * (lane >> 5) + k4, M - 1)];
+            pw[q4] = isq ? int2{0, 0} : locate(row0 + 32 * i + 8 * q4 + 4 * (lane >> 5) + k4);
 #pragma unroll
           for (int q4 = 0; q4 < 4; ++q4) {
             float y0[4], y1[4];

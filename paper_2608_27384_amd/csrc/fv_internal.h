@@ -140,7 +140,8 @@ struct QkvArgs {
   T* vtarena;           // this layer's values [Bmax][Hkv][dh][S] (transposed)
   const float* rcos;    // [S][dh/2]
   const float* rsin;
-  const int2* row_pos;  // [rows] (stream b, arena row len[b] + token)
+  const int* len;       // [B] valid prefix rows: token row r of stream b = r / tokens
+                        // goes to arena row len[b] + r - b * tokens
   int tokens, n_q_heads, n_kv_heads, head_dim, S;
 };
 
@@ -187,7 +188,6 @@ template <typename T>
 void launch_resid_norm(const float* part, int ks, float* h, const float* mod, int mod_ld,
                        int gate_off, int norm_off, int chunk_len, float eps, T* u, int rows,
                        int W, hipStream_t s);
-void launch_row_pos(const int* len, int2* row_pos, int rows, int tokens, hipStream_t s);
 template <typename T>
 void launch_adarms(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
                    float eps, T* u, int rows, int W, hipStream_t s);
@@ -288,7 +288,6 @@ struct Handle {
   void* q = nullptr; void* o = nullptr;                           // T [Bmax*T][Hq*dh]
   void* m = nullptr;                                              // T [Bmax*T][F]
   float* v = nullptr;                                             // [Bmax][K][C][A]
-  int2* row_pos = nullptr;                                        // [Bmax*T]
   void* part_o = nullptr; float* part_ml = nullptr; int max_split = 1;
   float* seq_x = nullptr; float* seq_t = nullptr;
   std::vector<std::pair<int, float*>> tscheds;  // sequential-decode t_j tables by step count

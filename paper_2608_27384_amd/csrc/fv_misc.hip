@@ -267,15 +267,6 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const float* __restrict
   }
 }
 
-// (stream, arena row) of every token row: b = row / tokens, len[b] + token.
-__global__ void row_pos_kernel(const int* __restrict__ len, int2* __restrict__ row_pos, int rows,
-                               int tokens) {
-  const int row = blockIdx.x * blockDim.x + threadIdx.x;
-  if (row >= rows) return;
-  const int b = row / tokens;
-  row_pos[row] = make_int2(b, len[b] + (row - b * tokens));
-}
-
 // -------------------------------------------------- FiLM-conditioned RMSNorm
 // u = h / sqrt(mean(h^2) + eps) * (1 + scale[chunk]) + shift[chunk]; one wave per row.
 template <typename T>
@@ -710,11 +701,6 @@ void launch_resid_norm(const float* part, int ks, float* h, const float* mod, in
                        int W, hipStream_t s) {
   hipLaunchKernelGGL((resid_norm_kernel<T>), dim3(rows), dim3(256), 0, s, part, ks, h, mod,
                      mod_ld, gate_off, norm_off, chunk_len, eps, u, rows, W);
-}
-
-void launch_row_pos(const int* len, int2* row_pos, int rows, int tokens, hipStream_t s) {
-  hipLaunchKernelGGL(row_pos_kernel, dim3((rows + 255) / 256), dim3(256), 0, s, len, row_pos,
-                     rows, tokens);
 }
 
 template <typename T>

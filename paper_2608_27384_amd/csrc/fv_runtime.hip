@@ -206,7 +206,6 @@ void enqueue_forward(Handle* h, const float* buffer, const float* t, int B, floa
     enqueue_film_maps<T>(h, t, B, h->mod, s);
     mod = h->mod;
   }
-  launch_row_pos(h->d_len, h->row_pos, rowsT, h->T, s);
   launch_embed_adarms<T>(buffer, h->w_in, h->b_in, h->hres, mod, Nmod, h->C, h->cfg.rms_eps,
                          (T*)h->u, rowsT, h->A, W, s);
   const int n_split = attn_split(h, B);
@@ -214,7 +213,7 @@ void enqueue_forward(Handle* h, const float* buffer, const float* t, int B, floa
     T* kar = (T*)h->karena + l * layer_elems;
     T* var = (T*)h->vtarena + l * layer_elems;
     const int n_attn = 2 * l, n_mlp = 2 * l + 1;
-    QkvArgs<T> qa{(T*)h->q, kar, var, h->rcos, h->rsin, h->row_pos, h->T, h->Hq, h->Hkv, h->dh,
+    QkvArgs<T> qa{(T*)h->q, kar, var, h->rcos, h->rsin, h->d_len, h->T, h->Hq, h->Hkv, h->dh,
                   h->S};
     gemm_qkv<T>((T*)h->u, (const T*)h->wqkv[l], qa, rowsT, h->Nqkv, W, h->gw, s);
     launch_attention<T>(attn_args(h, kar, var, B, n_split), s);
@@ -244,7 +243,7 @@ void run_stage(Handle* h, int stage, int l, hipStream_t s) {
       gemm_bias_f32<T>((T*)h->cond, (T*)h->w_mod, h->b_mod, h->mod, rowsK, h->Nmod, W, h->gw, s);
       break;
     case 1: {
-      QkvArgs<T> qa{(T*)h->q, kar, var, h->rcos, h->rsin, h->row_pos, h->T, h->Hq, h->Hkv,
+      QkvArgs<T> qa{(T*)h->q, kar, var, h->rcos, h->rsin, h->d_len, h->T, h->Hq, h->Hkv,
                     h->dh, h->S};
       gemm_qkv<T>((T*)h->u, (const T*)h->wqkv[l], qa, rowsT, h->Nqkv, W, h->gw, s);
       break;
@@ -612,7 +611,6 @@ fv_status fv_create(const fv_weights* w, const fv_cfg* cfg, fv_handle* out) {
     H.o = dalloc(h, rowsT * qd * H.esz);
     H.m = dalloc(h, rowsT * F * H.esz);
     H.v = static_cast<float*>(dalloc(h, rowsT * H.A * 4));
-    H.row_pos = static_cast<int2*>(dalloc(h, rowsT * sizeof(int2)));
     size_t part_rows = 0;
     for (int B = 1; B <= H.Bmax; ++B) {
       const int s = attn_split(h, B);

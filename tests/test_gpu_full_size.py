@@ -72,6 +72,24 @@ def test_velocity_parity_ragged_large_m():
         case.close()
 
 
+def test_velocity_parity_many_short_streams():
+    """90 streams of 50 tokens: 4500 rows take the 256-row GEMM tiles, whose
+    128-row wave slabs span three or four streams, so the QKV epilogue looks
+    every row's stream up instead of reading two prefix lengths."""
+    w = synth.workload("short_chunk").replace(name="short_b90", batch=90)
+    case = Case(w)
+    try:
+        v = case.gpu_velocity()
+        assert np.all(np.isfinite(v))
+        for b in (0, 45, w.batch - 1):
+            ref = case.oracle_velocity(b)
+            errs = [rel_err(v[b, k], ref[k]) for k in range(w.n_chunks)]
+            _say(f"short_b90 stream {b} (P={case.lens[b]}): max rel err {max(errs):.2e}")
+            assert max(errs) < tol(w), (b, errs)
+    finally:
+        case.close()
+
+
 def test_decode_steps_lockstep_pi05():
     """Two steps of the headline workload: emitted chunk within tolerance of
     the oracle, shifted slots bit-exact against the fp32 queue update of the
