@@ -851,29 +851,28 @@ __global__ __launch_bounds__(256) void gemv_bias_silu_kernel(const T* __restrict
 #pragma unroll
   for (int m = 0; m < kGemvRows; ++m) acc[m] = 0.f;
   const T* wrow = Bt + (size_t)n * K;
+  // rows m >= M re-read row M - 1 (in bounds, never stored), so every load
+  // is unconditional and all of a k-piece's loads go out before its FMAs
+#pragma unroll 2
   for (int k0 = EPV * lane; k0 < K; k0 += 64 * EPV) {
-    float wv[EPV];
-    {
-      const u32x4 raw = *reinterpret_cast<const u32x4*>(wrow + k0);
-      const T* e = reinterpret_cast<const T*>(&raw);
+    const u32x4 wraw = *reinterpret_cast<const u32x4*>(wrow + k0);
+    u32x4 araw[kGemvRows];
 #pragma unroll
-      for (int i = 0; i < EPV; ++i) wv[i] = to_f32(e[i]);
-    }
+    for (int m = 0; m < kGemvRows; ++m)
+      araw[m] = *reinterpret_cast<const u32x4*>(A + (size_t)min(m, M - 1) * K + k0);
+    const T* we = reinterpret_cast<const T*>(&wraw);
 #pragma unroll
     for (int m = 0; m < kGemvRows; ++m) {
-      if (m >= M) break;
-      const u32x4 raw = *reinterpret_cast<const u32x4*>(A + (size_t)m * K + k0);
-      const T* e = reinterpret_cast<const T*>(&raw);
+      const T* e = reinterpret_cast<const T*>(&araw[m]);
 #pragma unroll
-      for (int i = 0; i < EPV; ++i) acc[m] = fmaf(to_f32(e[i]), wv[i], acc[m]);
+      for (int i = 0; i < EPV; ++i) acc[m] = fmaf(to_f32(e[i]), to_f32(we[i]), acc[m]);
     }
   }
   const float b = bias[n];
 #pragma unroll
   for (int m = 0; m < kGemvRows; ++m) {
-    if (m >= M) break;
     const float v = wave_sum(acc[m]);
-    if (lane == 0) out[(size_t)m * N + n] = from_f32<T>(silu_f(v + b));
+    if (m < M && lane == 0) out[(size_t)m * N + n] = from_f32<T>(silu_f(v + b));
   }
 }
 
