@@ -3,9 +3,10 @@
 // The mask of the paper (Sec. 3.1: a noisier, later chunk attends to the
 // cleaner, earlier chunks, never the reverse, at chunk granularity; every
 // action token sees the cached observation) becomes two key ranges here:
-// the QKV epilogue writes buffer token j of stream b at arena row P_b + j,
-// right after the P_b valid prefix rows, so a query of chunk k sees the rows
-// [0, P_b) and [P_b + C lo, P_b + C hi) with (lo, hi) = (first valid slot,
+// the QKV epilogue writes buffer token j of stream b at arena row P0_b + j,
+// P0_b = buffer_row0(P_b) >= P_b the first multiple of 8 at or after the P_b
+// valid prefix rows, so a query of chunk k sees the rows [0, P_b) and
+// [P0_b + C lo, P0_b + C hi) with (lo, hi) = (first valid slot,
 // k + 1).  The other mask modes and cold-start padding only change (lo, hi)
 // (visible_chunks).  Keys outside a query's ranges are scored -inf, giving
 // probability exactly 0; tiles outside every row's ranges are not visited.
@@ -52,7 +53,7 @@ constexpr int rows_per_block() {
 }
 
 // Key tiles a block visits: the prefix tiles [0, nA), then the tiles of the
-// buffer span [P + C lo_min, P + C hi_max) (the rows' visible chunk ranges
+// buffer span [P0 + C lo_min, P0 + C hi_max) (the rows' visible chunk ranges
 // are monotone in the chunk index, so the first and last row of the block
 // bound them), without the masked gap between the two.
 struct KeyTiles {
@@ -61,13 +62,14 @@ struct KeyTiles {
 };
 __device__ __forceinline__ KeyTiles key_tiles(int P, int C, int K, int first, int mode,
                                               int tok_first, int tok_last, int KT) {
+  const int P0 = buffer_row0(P);  // arena row of the first buffer token
   int lo0, hi0, lo1, hi1;
   visible_chunks(tok_first / C, K, first, mode, lo0, hi0);
   visible_chunks(tok_last / C, K, first, mode, lo1, hi1);
   KeyTiles r;
   r.nA = (P + KT - 1) / KT;
-  r.tB0 = max((P + C * lo0) / KT, r.nA);
-  const int tB1 = (P + C * hi1 + KT - 1) / KT;
+  r.tB0 = max((P0 + C * lo0) / KT, r.nA);
+  const int tB1 = (P0 + C * hi1 + KT - 1) / KT;
   r.n = r.nA + max(0, tB1 - r.tB0);
   return r;
 }
@@ -115,8 +117,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     head[q] = g * G + (rqc - tok[q] * G);
     int lo, hi;
     visible_chunks(tok[q] / C, K, first, a.mask_mode, lo, hi);
-    klo[q] = P + C * lo;
-    khi[q] = P + C * hi;
+    klo[q] = buffer_row0(P) + C * lo;
+    khi[q] = buffer_row0(P) + C * hi;
   }
   const int rlast = min(tile0 + kRowsPerBlock - 1, rows_bg - 1);
   const KeyTiles kts = key_tiles(P, C, K, first, a.mask_mode, tile0 / G, rlast / G, KT);
@@ -422,8 +424,8 @@ __global__ __launch_bounds__(64 * NWV) void attn16_kernel(AttnArgs a) {
   const int head = g * G + (rqc - tok * G);
   int klo, khi;  // this row's visible buffer keys [klo, khi); prefix keys [0, P)
   visible_chunks(tok / C, K, first, a.mask_mode, klo, khi);
-  klo = P + C * klo;
-  khi = P + C * khi;
+  klo = buffer_row0(P) + C * klo;
+  khi = buffer_row0(P) + C * khi;
   const int rlast = min(tile0 + RB - 1, rows_bg - 1);
   const KeyTiles kts = key_tiles(P, C, K, first, a.mask_mode, tile0 / G, rlast / G, KT);
   const int kt_begin = (split * kts.n) / a.n_split, kt_end = ((split + 1) * kts.n) / a.n_split;
@@ -677,8 +679,8 @@ __global__ __launch_bounds__(64 * NWV) void attn16d_kernel(AttnArgs a) {
   const int head = g * G + (rqc - tok * G);
   int klo, khi;  // this row's visible buffer keys [klo, khi); prefix keys [0, P)
   visible_chunks(tok / C, K, first, a.mask_mode, klo, khi);
-  klo = P + C * klo;
-  khi = P + C * khi;
+  klo = buffer_row0(P) + C * klo;
+  khi = buffer_row0(P) + C * khi;
   const int rlast = min(tile0 + RB - 1, rows_bg - 1);
   const KeyTiles kts = key_tiles(P, C, K, first, a.mask_mode, tile0 / G, rlast / G, KT);
   const int kt_begin = (split * kts.n) / a.n_split, kt_end = ((split + 1) * kts.n) / a.n_split;

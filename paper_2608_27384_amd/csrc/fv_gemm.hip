@@ -33,7 +33,8 @@
 //  * bias + SiLU (time-MLP), bias to fp32 (FiLM maps);
 //  * QKV: queries and keys are rotated (half-split rotary pairs) and keys and
 //    values are written straight into the layer's K / V^T arena at row
-//    len[b] + token, so attention reads [prefix ; buffer] as one key range;
+//    buffer_row0(len[b]) + token (the prefix length rounded up to 8), so
+//    attention reads [prefix ; buffer] from one arena;
 //  * gated residual h += gate[chunk] * acc;
 //  * GeGLU gelu(g) * u and plain GELU.
 // Element-type outputs of the QKV and GELU epilogues are transposed within
@@ -606,14 +607,23 @@ struct EpiQkv {
     const int qd = a.n_q_heads * dh, kd = a.n_kv_heads * dh;
     const float* __restrict__ rcos = a.rcos;
     const float* __restrict__ rsin = a.rsin;
-    // (stream, arena row) of a token row: b = row / tokens, len[b] + row -
-    // b tokens.  The wave's rows span at most two streams when tokens >= 32
-    // FM: their two lengths are read once (no per-row lookup ahead of the
-    // rotary tables); otherwise every row looks its stream up.
+    // (stream, arena row) of a token row: b = row / tokens,
+    // buffer_row0(len[b]) + row - b tokens.  The wave's rows span at most two
+    // streams when tokens >= 32 FM: their two lengths are read once (no
+    // per-row lookup ahead of the rotary tables); otherwise every row looks
+    // its stream up.
     const int ntok = a.tokens;
     const int b_lo = min(row0, M - 1) / ntok, b_hi = min(row0 + 32 * FM - 1, M - 1) / ntok;
     const bool two = b_hi - b_lo <= 1;
-    const int len_lo = a.len[b_lo], len_hi = a.len[b_hi], row_hi = b_hi * ntok;
+    const int len_lo = buffer_row0(a.len[b_lo]), len_hi = buffer_row0(a.len[b_hi]);
+    const int gap_lo = len_lo - a.len[b_lo], gap_hi = len_hi - a.len[b_hi];
+    const int row_hi = b_hi * ntok;
+    // rotary position of a token = its arena row minus its stream's alignment gap
+    auto gap_of = [&](int b) __attribute__((always_inline)) {
+      if (two) return b == b_hi ? gap_hi : gap_lo;
+      const int P = a.len[b];
+      return buffer_row0(P) - P;
+    };
     auto locate = [&](int row) __attribute__((always_inline)) {
       row = min(row, M - 1);
       if (two) {
@@ -622,7 +632,7 @@ struct EpiQkv {
         return int2{b, (hi ? len_hi : len_lo) + row - b * ntok};
       }
       const int b = row / ntok;
-      return int2{b, a.len[b] + row - b * ntok};
+      return int2{b, buffer_row0(a.len[b]) + row - b * ntok};
     };
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
@@ -640,8 +650,9 @@ struct EpiQkv {
           float cs[16], sn[16];
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            cs[r] = rcos[(size_t)rp[r].y * half + dlo];
-            sn[r] = rsin[(size_t)rp[r].y * half + dlo];
+            const int pos = rp[r].y - gap_of(rp[r].x);
+            cs[r] = rcos[(size_t)pos * half + dlo];
+            sn[r] = rsin[(size_t)pos * half + dlo];
           }
           // rotated pair (d, d + dh/2) per register, then each group of
           // four rows transposed so a lane writes 4 features of one row

@@ -141,7 +141,7 @@ struct QkvArgs {
   const float* rcos;    // [S][dh/2]
   const float* rsin;
   const int* len;       // [B] valid prefix rows: token row r of stream b = r / tokens
-                        // goes to arena row len[b] + r - b * tokens
+                        // goes to arena row buffer_row0(len[b]) + r - b * tokens
   int tokens, n_q_heads, n_kv_heads, head_dim, S;
 };
 
@@ -206,6 +206,12 @@ template <typename T>
 void launch_prefix_copy(const T* k, const T* v, int L, int B, int src_batch, int ld, int Hkv,
                         int dh, T* karena, T* vtarena, int Bmax, int S, const int* len,
                         hipStream_t s);
+
+// Arena row of a stream's first buffer token: the prefix length rounded up
+// to a multiple of 8, so the QKV epilogue's runs of four tokens of V^T (8
+// bytes) start aligned for every prefix length.  Rows [P, buffer_row0(P))
+// hold zeros or an earlier prefix's finite values and are never visible.
+__host__ __device__ __forceinline__ int buffer_row0(int P) { return (P + 7) & ~7; }
 
 struct AttnArgs {
   const void* q;        // [B*tokens][Hq][dh]

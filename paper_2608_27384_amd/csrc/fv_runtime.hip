@@ -478,7 +478,7 @@ fv_status fv_create(const fv_weights* w, const fv_cfg* cfg, fv_handle* out) {
     H.L = cfg->n_layers; H.W = cfg->width; H.Hq = cfg->n_q_heads; H.Hkv = cfg->n_kv_heads;
     H.dh = cfg->head_dim; H.F = cfg->mlp_dim; H.A = cfg->action_dim; H.C = cfg->chunk_len;
     H.K = cfg->n_chunks; H.T = H.K * H.C; H.Pmax = cfg->max_prefix; H.Bmax = cfg->max_batch;
-    H.S = ((H.Pmax + H.T + 63) / 64) * 64;
+    H.S = ((buffer_row0(H.Pmax) + H.T + 63) / 64) * 64;
     H.Nqkv = (H.Hq + 2 * H.Hkv) * H.dh;
     H.Nmod = (6 * H.L + 2) * H.W;
     H.Ngu = cfg->mlp_gated ? 2 * H.F : H.F;
