@@ -370,6 +370,8 @@ constexpr int dma_lds_bytes() {
   return NS * (BM + BN) * 128;
 }
 
+struct EpiNone;  // partials only (split-K feeding the fused residual reduction)
+
 template <int BM, int BN, int NW, int WGM, int NS, class Epi>
 __global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(const bf16_t* __restrict__ A,
                                                            const bf16_t* __restrict__ Bt, int M,
@@ -492,18 +494,37 @@ __global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(const bf16_t* __restr
   }
   const int ar = wm * WTM, bc = wn * WTN;
   if (KS > 1) {
-    float* part = ws + (size_t)kz * M * N;
+    if constexpr (std::is_same<Epi, EpiNone>::value) {
+      // partials for the fused residual reduction: bf16, four columns of a
+      // row per store (the sum over splits and the residual stay fp32)
+      bf16_t* part = reinterpret_cast<bf16_t*>(ws) + (size_t)kz * M * N;
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+      for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int col = n0 + bc + 32 * j + lr;
+        for (int j = 0; j < FN; ++j) {
+          const int col = n0 + bc + 32 * j + (lane & 28);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = m0 + ar + 32 * i + acc_row(r, lane);
-          if (row < M) part[(size_t)row * N + col] = acc[i][j][r];
+          for (int q4 = 0; q4 < 4; ++q4) {
+            const f32x4 u = quad_rows(acc[i][j][4 * q4], acc[i][j][4 * q4 + 1],
+                                      acc[i][j][4 * q4 + 2], acc[i][j][4 * q4 + 3], lane);
+            const int row = m0 + ar + 32 * i + 8 * q4 + 4 * (lane >> 5) + (lane & 3);
+            if (row < M) store4<bf16_t>(part + (size_t)row * N + col, u[0], u[1], u[2], u[3]);
+          }
         }
-      }
+    } else {
+      float* part = ws + (size_t)kz * M * N;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int col = n0 + bc + 32 * j + lr;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = m0 + ar + 32 * i + acc_row(r, lane);
+            if (row < M) part[(size_t)row * N + col] = acc[i][j][r];
+          }
+        }
+    }
     return;
   }
   if constexpr (epi_staged<Epi>()) {
@@ -1010,11 +1031,15 @@ GemmPlan plan_gemm(int M, int N, int K, bool bf16) {
 
 template <typename T>
 int gemm_partials(const T* A, const T* Bt, int M, int N, int K, const GemmWork& w,
-                  hipStream_t s) {
+                  hipStream_t s, bool* bf16_parts) {
   const GemmPlan p = plan_gemm(M, N, K, sizeof(T) == 2);
+  *bf16_parts = false;
   if (p.ks <= 1) return 1;
   if constexpr (sizeof(T) == 2) {
-    if (try_dma(A, Bt, M, N, K, p, w, EpiNone{}, s)) return p.ks;
+    if (try_dma(A, Bt, M, N, K, p, w, EpiNone{}, s)) {
+      *bf16_parts = true;
+      return p.ks;
+    }
   }
   switch (p.tile) {
     case T256x128w8: launch_tile<T, 256, 128, 8, 4, kTileKG[0]>(A, Bt, M, N, K, p, w, EpiNone{}, s); break;
@@ -1096,7 +1121,8 @@ hipError_t gemm_prepare() {
   template void gemm_geglu<T>(const T*, const T*, T*, int, int, int, const GemmWork&,            \
                               hipStream_t);                                                      \
   template void gemm_gelu<T>(const T*, const T*, T*, int, int, int, const GemmWork&, hipStream_t); \
-  template int gemm_partials<T>(const T*, const T*, int, int, int, const GemmWork&, hipStream_t);
+  template int gemm_partials<T>(const T*, const T*, int, int, int, const GemmWork&, hipStream_t, \
+                                bool*);
 FV_INSTANTIATE(bf16_t)
 FV_INSTANTIATE(float)
 #undef FV_INSTANTIATE

@@ -169,11 +169,12 @@ void gemm_gelu(const T* A, const T* Bt, T* out, int M, int N, int K, const GemmW
 // Raises the dynamic LDS limit of the large-M GEMM kernels (call once per
 // device before the first GEMM launch).
 hipError_t gemm_prepare();
-// Split-K GEMM that only writes its fp32 partials [KS][M][N] to w.ws; returns
-// KS, or 1 (nothing launched) when the plan does not split k.
+// Split-K GEMM that only writes its partials [KS][M][N] to w.ws; returns KS,
+// or 1 (nothing launched) when the plan does not split k.  *bf16_parts: the
+// partials are bf16 (the direct-to-LDS tiles), else fp32.
 template <typename T>
 int gemm_partials(const T* A, const T* Bt, int M, int N, int K, const GemmWork& w,
-                  hipStream_t s);
+                  hipStream_t s, bool* bf16_parts);
 
 // ------------------------------------------------------------ other kernels
 template <typename T>
@@ -184,10 +185,11 @@ void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, f
                          int A, int W, hipStream_t s);
 // h += gate * sum_z part[z] (split order); then, if norm_off >= 0,
 // u = rmsnorm(h) (1 + scale) + shift with the modulation at norm_off.
+// part holds bf16 values when bf16_parts, else fp32.
 template <typename T>
-void launch_resid_norm(const float* part, int ks, float* h, const float* mod, int mod_ld,
-                       int gate_off, int norm_off, int chunk_len, float eps, T* u, int rows,
-                       int W, hipStream_t s);
+void launch_resid_norm(const void* part, bool bf16_parts, int ks, float* h, const float* mod,
+                       int mod_ld, int gate_off, int norm_off, int chunk_len, float eps, T* u,
+                       int rows, int W, hipStream_t s);
 template <typename T>
 void launch_adarms(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
                    float eps, T* u, int rows, int W, hipStream_t s);

@@ -208,10 +208,11 @@ __global__ __launch_bounds__(256) void embed_adarms_rows_kernel(
 }
 
 // --------------------------------------- gated residual + next FiLM RMSNorm
-// One block per row: h[row] += gate[chunk] * sum_z part[z][row] (split order),
-// then (norm_off >= 0) u[row] = rmsnorm(h) (1 + scale) + shift.
-template <typename T>
-__global__ __launch_bounds__(256) void resid_norm_kernel(const float* __restrict__ part, int ks,
+// One block per row: h[row] += gate[chunk] * sum_z part[z][row] (split order,
+// fp32 sums of the partials, which are stored as P), then (norm_off >= 0)
+// u[row] = rmsnorm(h) (1 + scale) + shift.
+template <typename T, typename P>
+__global__ __launch_bounds__(256) void resid_norm_kernel(const P* __restrict__ part, int ks,
                                                          float* __restrict__ h,
                                                          const float* __restrict__ mod,
                                                          int mod_ld, int gate_off, int norm_off,
@@ -229,7 +230,7 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const float* __restrict
       f32x4 pz[8];  // every split's load issued before the sum (ks <= 8)
 #pragma unroll
       for (int z = 0; z < 8; ++z)
-        pz[z] = z < ks ? *reinterpret_cast<const f32x4*>(part + ((size_t)z * rows + row) * W + c)
+        pz[z] = z < ks ? load4_f32(part + ((size_t)z * rows + row) * W + c)
                        : f32x4{0.f, 0.f, 0.f, 0.f};
       const f32x4 g = *reinterpret_cast<const f32x4*>(mrow + gate_off + c);
       f32x4 hv = *reinterpret_cast<const f32x4*>(h + (size_t)row * W + c);
@@ -696,11 +697,17 @@ void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, f
 }
 
 template <typename T>
-void launch_resid_norm(const float* part, int ks, float* h, const float* mod, int mod_ld,
-                       int gate_off, int norm_off, int chunk_len, float eps, T* u, int rows,
-                       int W, hipStream_t s) {
-  hipLaunchKernelGGL((resid_norm_kernel<T>), dim3(rows), dim3(256), 0, s, part, ks, h, mod,
-                     mod_ld, gate_off, norm_off, chunk_len, eps, u, rows, W);
+void launch_resid_norm(const void* part, bool bf16_parts, int ks, float* h, const float* mod,
+                       int mod_ld, int gate_off, int norm_off, int chunk_len, float eps, T* u,
+                       int rows, int W, hipStream_t s) {
+  if (bf16_parts)
+    hipLaunchKernelGGL((resid_norm_kernel<T, bf16_t>), dim3(rows), dim3(256), 0, s,
+                       static_cast<const bf16_t*>(part), ks, h, mod, mod_ld, gate_off, norm_off,
+                       chunk_len, eps, u, rows, W);
+  else
+    hipLaunchKernelGGL((resid_norm_kernel<T, float>), dim3(rows), dim3(256), 0, s,
+                       static_cast<const float*>(part), ks, h, mod, mod_ld, gate_off, norm_off,
+                       chunk_len, eps, u, rows, W);
 }
 
 template <typename T>
@@ -774,10 +781,10 @@ template void launch_embed_adarms<bf16_t>(const float*, const float*, const floa
 template void launch_embed_adarms<float>(const float*, const float*, const float*, float*,
                                          const float*, int, int, float, float*, int, int, int,
                                          hipStream_t);
-template void launch_resid_norm<bf16_t>(const float*, int, float*, const float*, int, int, int,
-                                        int, float, bf16_t*, int, int, hipStream_t);
-template void launch_resid_norm<float>(const float*, int, float*, const float*, int, int, int,
-                                       int, float, float*, int, int, hipStream_t);
+template void launch_resid_norm<bf16_t>(const void*, bool, int, float*, const float*, int, int,
+                                        int, int, float, bf16_t*, int, int, hipStream_t);
+template void launch_resid_norm<float>(const void*, bool, int, float*, const float*, int, int,
+                                       int, int, float, float*, int, int, hipStream_t);
 template void launch_adarms<bf16_t>(const float*, const float*, int, int, int, float, bf16_t*,
                                     int, int, hipStream_t);
 template void launch_adarms<float>(const float*, const float*, int, int, int, float, float*, int,

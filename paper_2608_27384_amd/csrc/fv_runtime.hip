@@ -165,10 +165,11 @@ template <typename T>
 void resid_block(Handle* h, const float* mod, const T* A, const T* Bt, int K, int gate_off,
                  int norm_off, int rowsT, hipStream_t s) {
   const int W = h->W;
-  const int ks = gemm_partials<T>(A, Bt, rowsT, W, K, h->gw, s);
+  bool bf16_parts = false;
+  const int ks = gemm_partials<T>(A, Bt, rowsT, W, K, h->gw, s, &bf16_parts);
   if (ks > 1) {
-    launch_resid_norm<T>(h->gw.ws, ks, h->hres, mod, h->Nmod, gate_off, norm_off, h->C,
-                         h->cfg.rms_eps, (T*)h->u, rowsT, W, s);
+    launch_resid_norm<T>(h->gw.ws, bf16_parts, ks, h->hres, mod, h->Nmod, gate_off, norm_off,
+                         h->C, h->cfg.rms_eps, (T*)h->u, rowsT, W, s);
   } else {
     gemm_gated_resid<T>(A, Bt, h->hres, mod, h->Nmod, gate_off, h->C, rowsT, W, K, h->gw, s);
     if (norm_off >= 0)
