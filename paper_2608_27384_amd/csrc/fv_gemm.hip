@@ -951,9 +951,11 @@ void launch_dma(const bf16_t* A, const bf16_t* Bt, int M, int N, int K, const Ge
   dim3 grid(N / BN, (M + BM - 1) / BM, p.ks);
   hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, NW, WGM, NS, Epi>), grid, dim3(64 * NW),
                      (dma_lds_bytes<BM, BN, NW, WGM, NS>()), s, A, Bt, M, N, K, p.ks, w.ws, epi);
-  if (p.ks > 1 && !std::is_same<Epi, EpiNone>::value)
-    hipLaunchKernelGGL((gemm_reduce_kernel<BM, BN, NW, WGM, Epi>), dim3(grid.x, grid.y),
-                       dim3(64 * NW), 0, s, w.ws, M, N, p.ks, epi);
+  // the 256x256 tile never splits k (plan_gemm), so it has no reduction
+  if constexpr (BM * BN < 256 * 256 && !std::is_same<Epi, EpiNone>::value)
+    if (p.ks > 1)
+      hipLaunchKernelGGL((gemm_reduce_kernel<BM, BN, NW, WGM, Epi>), dim3(grid.x, grid.y),
+                         dim3(64 * NW), 0, s, w.ws, M, N, p.ks, epi);
 }
 
 // Launches tile p.tile with the direct-to-LDS kernel when it has one;
