@@ -678,7 +678,7 @@ struct EpiQkv {
           // rotated pair (d, d + dh/2) per register, then each group of
           // four rows transposed so a lane writes 4 features of one row
           const int d0 = dlo & ~3, k4 = lane & 3;
-          // (stream, position) of the row each lane writes (K rows only)
+          // (stream, arena row) of the row each lane writes (K rows only)
           int2 pw[4];
 #pragma unroll
           for (int q4 = 0; q4 < 4; ++q4)
