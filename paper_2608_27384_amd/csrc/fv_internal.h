@@ -101,6 +101,34 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
+// Pulls part of [p, p + bytes) into the chip's memory-side cache ahead of
+// the kernel that reads it next (the weights of the next GEMM, which would
+// otherwise come cold from HBM): thread t of the grid loads the 16-byte
+// pieces t, t + n, .. (NPF of them, n = the grid's threads) at its kernel's
+// start and discards them at the end, so the loads overlap the kernel's own
+// work.  Reads only inside the buffer; p == nullptr loads nothing.
+template <int NPF>
+struct Prefetch {
+  u32x4 v[NPF];
+  __device__ __forceinline__ void issue(const void* p, size_t bytes) {
+    const size_t n = (size_t)gridDim.x * gridDim.y * gridDim.z * blockDim.x;
+    const size_t t =
+        (((size_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x) * blockDim.x +
+        threadIdx.x;
+    const u32x4* q = static_cast<const u32x4*>(p);
+    const size_t np = p ? bytes / 16 : 0;
+#pragma unroll
+    for (int i = 0; i < NPF; ++i) {
+      const size_t k = t + (size_t)i * n;
+      v[i] = k < np ? q[k] : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  __device__ __forceinline__ void retire() const {
+#pragma unroll
+    for (int i = 0; i < NPF; ++i) asm volatile("" ::"v"(v[i]));
+  }
+};
+
 // Both activations are evaluated as x / (1 + 2^a) with the bare hardware
 // exp2 and reciprocal instructions (1 ulp each; a few instructions instead
 // of the library tanh, and instead of the range handling of exp2f and the
@@ -185,11 +213,13 @@ void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, f
                          int A, int W, hipStream_t s);
 // h += gate * sum_z part[z] (split order); then, if norm_off >= 0,
 // u = rmsnorm(h) (1 + scale) + shift with the modulation at norm_off.
-// part holds bf16 values when bf16_parts, else fp32.
+// part holds bf16 values when bf16_parts, else fp32.  [pf, pf + pf_bytes)
+// (the next GEMM's weights, or nullptr) is pulled into the memory-side cache
+// meanwhile.
 template <typename T>
 void launch_resid_norm(const void* part, bool bf16_parts, int ks, float* h, const float* mod,
                        int mod_ld, int gate_off, int norm_off, int chunk_len, float eps, T* u,
-                       int rows, int W, hipStream_t s);
+                       int rows, int W, const void* pf, size_t pf_bytes, hipStream_t s);
 template <typename T>
 void launch_adarms(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
                    float eps, T* u, int rows, int W, hipStream_t s);
@@ -226,6 +256,8 @@ struct AttnArgs {
   int B, tokens, chunk_len, n_q_heads, n_kv_heads, head_dim, S, n_split;
   const int* n_valid;   // [B] non-padding slots per stream (the last n_valid slots)
   int mask_mode;        // FV_MASK_*
+  const void* pf;       // prefetched into the memory-side cache meanwhile (or nullptr)
+  size_t pf_bytes;
 };
 
 // Buffer chunks [lo, hi) visible to the queries of chunk kq (see the mask

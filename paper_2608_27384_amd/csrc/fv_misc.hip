@@ -217,9 +217,12 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const P* __restrict__ p
                                                          const float* __restrict__ mod,
                                                          int mod_ld, int gate_off, int norm_off,
                                                          int chunk_len, float eps,
-                                                         T* __restrict__ u, int rows, int W) {
+                                                         T* __restrict__ u, int rows, int W,
+                                                         const void* pf, size_t pf_bytes) {
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x;
+  Prefetch<8> pre;
+  pre.issue(pf, pf_bytes);
   const float* mrow = mod + (size_t)(row / chunk_len) * mod_ld;
   f32x4 hq[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
   float ss = 0.f;
@@ -244,7 +247,10 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const P* __restrict__ p
       ss += hv[0] * hv[0] + hv[1] * hv[1] + hv[2] * hv[2] + hv[3] * hv[3];
     }
   }
-  if (norm_off < 0) return;
+  if (norm_off < 0) {
+    pre.retire();
+    return;
+  }
   f32x4 svq[2], bvq[2];  // the norm's maps are requested before the row sum waits
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
@@ -266,6 +272,7 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const P* __restrict__ p
                 hv[3] * rinv * (1.0f + sv[3]) + bv[3]);
     }
   }
+  pre.retire();
 }
 
 // -------------------------------------------------- FiLM-conditioned RMSNorm
@@ -699,15 +706,15 @@ void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, f
 template <typename T>
 void launch_resid_norm(const void* part, bool bf16_parts, int ks, float* h, const float* mod,
                        int mod_ld, int gate_off, int norm_off, int chunk_len, float eps, T* u,
-                       int rows, int W, hipStream_t s) {
+                       int rows, int W, const void* pf, size_t pf_bytes, hipStream_t s) {
   if (bf16_parts)
     hipLaunchKernelGGL((resid_norm_kernel<T, bf16_t>), dim3(rows), dim3(256), 0, s,
                        static_cast<const bf16_t*>(part), ks, h, mod, mod_ld, gate_off, norm_off,
-                       chunk_len, eps, u, rows, W);
+                       chunk_len, eps, u, rows, W, pf, pf_bytes);
   else
     hipLaunchKernelGGL((resid_norm_kernel<T, float>), dim3(rows), dim3(256), 0, s,
                        static_cast<const float*>(part), ks, h, mod, mod_ld, gate_off, norm_off,
-                       chunk_len, eps, u, rows, W);
+                       chunk_len, eps, u, rows, W, pf, pf_bytes);
 }
 
 template <typename T>
@@ -782,9 +789,11 @@ template void launch_embed_adarms<float>(const float*, const float*, const float
                                          const float*, int, int, float, float*, int, int, int,
                                          hipStream_t);
 template void launch_resid_norm<bf16_t>(const void*, bool, int, float*, const float*, int, int,
-                                        int, int, float, bf16_t*, int, int, hipStream_t);
+                                        int, int, float, bf16_t*, int, int, const void*, size_t,
+                                        hipStream_t);
 template void launch_resid_norm<float>(const void*, bool, int, float*, const float*, int, int,
-                                       int, int, float, float*, int, int, hipStream_t);
+                                       int, int, float, float*, int, int, const void*, size_t,
+                                       hipStream_t);
 template void launch_adarms<bf16_t>(const float*, const float*, int, int, int, float, bf16_t*,
                                     int, int, hipStream_t);
 template void launch_adarms<float>(const float*, const float*, int, int, int, float, float*, int,

@@ -161,15 +161,22 @@ int attn_split(const Handle* h, int B) {
 // ------------------------------------------------------------------ forward
 // Output projection / down projection with the gated residual, fused with
 // the FiLM RMSNorm that feeds the next GEMM (norm_off < 0: none).
+// Kernels ahead of a GEMM pull its weights into the memory-side cache.
+#ifndef FV_PREFETCH
+#define FV_PREFETCH 1
+#endif
+
 template <typename T>
 void resid_block(Handle* h, const float* mod, const T* A, const T* Bt, int K, int gate_off,
-                 int norm_off, int rowsT, hipStream_t s) {
+                 int norm_off, int rowsT, hipStream_t s, const void* next_w = nullptr,
+                 size_t next_bytes = 0) {
   const int W = h->W;
   bool bf16_parts = false;
   const int ks = gemm_partials<T>(A, Bt, rowsT, W, K, h->gw, s, &bf16_parts);
   if (ks > 1) {
     launch_resid_norm<T>(h->gw.ws, bf16_parts, ks, h->hres, mod, h->Nmod, gate_off, norm_off,
-                         h->C, h->cfg.rms_eps, (T*)h->u, rowsT, W, s);
+                         h->C, h->cfg.rms_eps, (T*)h->u, rowsT, W,
+                         FV_PREFETCH ? next_w : nullptr, next_bytes, s);
   } else {
     gemm_gated_resid<T>(A, Bt, h->hres, mod, h->Nmod, gate_off, h->C, rowsT, W, K, h->gw, s);
     if (norm_off >= 0)
@@ -189,9 +196,14 @@ void enqueue_film_maps(Handle* h, const float* t, int B, float* mod, hipStream_t
   gemm_bias_f32<T>((T*)h->cond, (T*)h->w_mod, h->b_mod, mod, rowsK, h->Nmod, W, h->gw, s);
 }
 
-AttnArgs attn_args(const Handle* h, const void* kar, const void* var, int B, int n_split) {
-  return AttnArgs{h->q, kar, var, h->d_len, h->o, h->part_o, h->part_ml, B, h->T, h->C, h->Hq,
-                  h->Hkv, h->dh, h->S, n_split, h->d_valid, h->mask_mode};
+// pf: the weights the next kernels read, pulled into the memory-side cache by
+// the attention (nullptr: none)
+AttnArgs attn_args(const Handle* h, const void* kar, const void* var, int B, int n_split,
+                   const void* pf = nullptr, size_t pf_bytes = 0) {
+  return AttnArgs{h->q,  kar,      var,  h->d_len, h->o,          h->part_o,
+                  h->part_ml, B,   h->T, h->C,     h->Hq,         h->Hkv,
+                  h->dh, h->S,     n_split, h->d_valid, h->mask_mode, FV_PREFETCH ? pf : nullptr,
+                  pf_bytes};
 }
 
 // Velocity pass.  `mod_cached` (FiLM maps of a static schedule) replaces the
@@ -217,16 +229,22 @@ void enqueue_forward(Handle* h, const float* buffer, const float* t, int B, floa
     QkvArgs<T> qa{(T*)h->q, kar, var, h->rcos, h->rsin, h->d_len, h->T, h->Hq, h->Hkv, h->dh,
                   h->S};
     gemm_qkv<T>((T*)h->u, (const T*)h->wqkv[l], qa, rowsT, h->Nqkv, W, h->gw, s);
-    launch_attention<T>(attn_args(h, kar, var, B, n_split), s);
+    // each kernel ahead of a GEMM pulls that GEMM's weights into the
+    // memory-side cache while it runs
+    launch_attention<T>(attn_args(h, kar, var, B, n_split, h->wo[l],
+                                  (size_t)W * h->Hq * h->dh * h->esz),
+                        s);
     resid_block<T>(h, mod, (const T*)h->o, (const T*)h->wo[l], h->Hq * h->dh,
-                   n_attn * 3 * W + 2 * W, n_mlp * 3 * W, rowsT, s);
+                   n_attn * 3 * W + 2 * W, n_mlp * 3 * W, rowsT, s, h->wgu[l],
+                   (size_t)h->Ngu * W * h->esz);
     if (h->cfg.mlp_gated)
       gemm_geglu<T>((T*)h->u, (const T*)h->wgu[l], (T*)h->m, rowsT, h->Ngu, W, h->gw, s);
     else
       gemm_gelu<T>((T*)h->u, (const T*)h->wgu[l], (T*)h->m, rowsT, h->Ngu, W, h->gw, s);
     const int next_norm = l + 1 < h->L ? 2 * (l + 1) * 3 * W : -1;
     resid_block<T>(h, mod, (const T*)h->m, (const T*)h->wd[l], h->F, n_mlp * 3 * W + 2 * W,
-                   next_norm, rowsT, s);
+                   next_norm, rowsT, s, l + 1 < h->L ? h->wqkv[l + 1] : nullptr,
+                   (size_t)h->Nqkv * W * h->esz);
   }
   if (v_out)
     launch_final(h->hres, mod, Nmod, 6 * h->L * W, h->C, h->cfg.rms_eps, h->w_out, h->b_out,
