@@ -77,6 +77,11 @@ def rmsnorm(h: np.ndarray, eps: float) -> np.ndarray:
     return h / np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + eps)
 
 
+def _as(a, dtype) -> np.ndarray:
+    """``a`` as an array of ``dtype`` (no copy when it already is one)."""
+    return np.asarray(a, dtype=dtype)
+
+
 def softmax_rows(s: np.ndarray) -> np.ndarray:
     """Row softmax over the last axis."""
     m = np.max(s, axis=-1, keepdims=True)
@@ -105,15 +110,15 @@ def timestep_embedding(t: float, width: int, dtype=np.float64,
 def time_condition(t: float, w: Dict, width: int, dtype=np.float64) -> np.ndarray:
     """cond = silu(silu(e W_t1 + b_t1) W_t2 + b_t2) for one chunk's noise level."""
     e = timestep_embedding(t, width, dtype)
-    hid = silu(e @ w["w_t1"].astype(dtype) + w["b_t1"].astype(dtype))
-    return silu(hid @ w["w_t2"].astype(dtype) + w["b_t2"].astype(dtype))
+    hid = silu(e @ _as(w["w_t1"], dtype) + _as(w["b_t1"], dtype))
+    return silu(hid @ _as(w["w_t2"], dtype) + _as(w["b_t2"], dtype))
 
 
 def film(cond: np.ndarray, w_mod: np.ndarray, b_mod: np.ndarray,
          dtype=np.float64) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
     """One norm's FiLM parameters: [scale | shift | gate] = cond M_n + m_n."""
     W = cond.shape[-1]
-    y = cond @ w_mod.astype(dtype) + b_mod.astype(dtype)
+    y = cond @ _as(w_mod, dtype) + _as(b_mod, dtype)
     return y[:W], y[W:2 * W], y[2 * W:3 * W]
 
 
@@ -178,14 +183,6 @@ def visible_chunks(chunk: int, n_chunks: int, first_valid: int = 0,
     if mode == "causal":
         return first_valid, chunk + 1
     return first_valid, n_chunks
-
-
-def visible_keys(chunk: int, chunk_len: int, prefix_len: int) -> Tuple[int, int]:
-    """Visible key set J(chunk) of the causal mask with a full buffer: all
-    valid prefix tokens and buffer tokens of chunks 0..chunk.  Returned as
-    (prefix count, buffer-token count)."""
-    lo, hi = visible_chunks(chunk, chunk + 1)
-    return prefix_len, (hi - lo) * chunk_len
 
 
 def chunk_causal_attention(q: np.ndarray, k_buf: np.ndarray, v_buf: np.ndarray,
@@ -253,7 +250,7 @@ def velocity(x: np.ndarray, t: np.ndarray, prefix_k: np.ndarray, prefix_v: np.nd
     Hq, Hkv, dh = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
     eps = cfg.rms_eps
     T = K * C
-    f = lambda a: np.asarray(a).astype(dtype)
+    f = lambda a: _as(a, dtype)
 
     # Time conditioning: one condition vector per chunk, and per norm the
     # FiLM [scale | shift | gate] triple of every chunk.
