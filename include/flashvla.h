@@ -137,9 +137,13 @@ fv_status fv_create(const fv_weights *weights, const fv_cfg *cfg, fv_handle *out
  *  len_host host int32 [batch]: valid prefix length of stream b, 0..max_prefix.
  *  batch    number of streams for the following steps, 1..max_batch.
  *  ld       leading row count of k/v, >= max(len_host).
- * The data are copied, stream-ordered, into the handle's arena, so k and v
- * may be reused once `stream` passes this point.  Sets the active batch.
- * Errors: FV_ERR_INVALID_ARG (NULL pointer, batch, ld or a length out of range).
+ * The data are copied into the handle's arena on `stream`, and the call
+ * waits for that copy to finish before it returns (host-synchronous), so k,
+ * v and len_host may be reused as soon as it returns; fv_set_prefix_async is
+ * the asynchronous form.  Sets the active batch and cancels a pending
+ * fv_set_prefix_async observation.
+ * Errors: FV_ERR_INVALID_ARG (NULL pointer, batch, ld or a length out of range),
+ * FV_ERR_HIP; after FV_ERR_INVALID_ARG the handle is unchanged.
  */
 fv_status fv_set_prefix(fv_handle h, const void *k, const void *v, const int32_t *len_host,
                         int32_t batch, int32_t ld, void *stream);
@@ -180,7 +184,9 @@ fv_status fv_set_prefix_async(fv_handle h, const void *k, const void *v, const i
  * A stream in cold start (fewer than K valid slots, see fv_cold_start) pops
  * a padding slot: its out_chunk is all zeros (the caller executes its safe
  * default action) and it gains one valid slot.
- * buffer and out_chunk must not overlap.  The first call with a new set of
+ * buffer and out_chunk must not overlap (FV_ERR_INVALID_ARG).  A staged
+ * fv_set_prefix_async observation is switched to only after every check has
+ * passed.  The first call with a new set of
  * pointers captures a HIP graph (host-synchronous); later calls replay it.
  * Errors: FV_ERR_STATE (no prefix set; t_per_chunk NULL without a schedule
  * for the active batch), FV_ERR_INVALID_ARG (NULL or misaligned pointer:
@@ -195,7 +201,7 @@ fv_status fv_decode_step(fv_handle h, float *buffer, const float *t_per_chunk, f
  *  NULL: the installed schedule), v_out dev fp32 [batch][K][C][A].  Uses the
  *  current mask mode and each stream's padding slots like fv_decode_step.
  * Same kernels, same order and same results as the pass inside fv_decode_step.
- * Errors: as fv_decode_step.
+ * buffer and v_out must not overlap.  Errors: as fv_decode_step.
  */
 fv_status fv_velocity(fv_handle h, const float *buffer, const float *t, float *v_out,
                       void *stream);

@@ -657,8 +657,8 @@ __global__ __launch_bounds__(64 * NWV) void attn16d_kernel(AttnArgs a) {
   extern __shared__ __attribute__((aligned(16))) T attn_ring[];
   unsigned char* ring = reinterpret_cast<unsigned char*>(attn_ring);
 
-  Prefetch<2> pre;  // the output projection's weights, into the memory-side cache
-  pre.issue(a.pf, a.pf_bytes);
+  Prefetch<2, NT> pre;  // the output projection's weights, into the memory-side cache
+  pre.issue(a.pf, a.pf_bytes, a.len);
   const int G = a.n_q_heads / a.n_kv_heads;
   const int rows_bg = a.tokens * G;
   int rtile, bg;

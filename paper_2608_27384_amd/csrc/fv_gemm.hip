@@ -23,9 +23,12 @@
 // each of the chip's 8 dies runs together on shared operands.
 //
 // Split-K (KS > 1): block z of a tile accumulates k-tiles [z*nk/KS,
-// (z+1)*nk/KS) and writes its fp32 partial tile to a workspace; a second,
-// small kernel sums the KS partials of each tile in split order (so the
-// result does not depend on scheduling) and runs the epilogue.  The kernel
+// (z+1)*nk/KS) and writes its partial tile to a workspace; a second, small
+// kernel sums the KS partials of each tile in split order (so the result
+// does not depend on scheduling) and runs the epilogue.  The partials are
+// fp32, except those of the direct-to-LDS kernel with no epilogue (EpiNone,
+// the output and down projections), which are bf16 and are summed by the
+// fused residual reduction (resid_norm_kernel).  The kernel
 // boundary makes the partials visible across the chip's separate L2 caches
 // without device-wide cache flushes inside the GEMM.
 //
@@ -348,8 +351,9 @@ constexpr bool epi_staged() { return EpiStaged<Epi>::value; }
 // multiplied.  Fragments of k-step s + LA are read during the MFMAs of
 // k-step s (LA = 2 for the 32x64 wave tiles, 1 for 128x64), so the barrier
 // comes LA - 1 k-steps before the end of a tile, once the wave has issued
-// its last read of it.  Split-K (KS > 1) writes fp32 partials as gemm_kernel
-// does.
+// its last read of it.  Split-K (KS > 1) with EpiNone writes bf16 partials,
+// four columns of a row per store (summed in fp32 by resid_norm_kernel);
+// with any other epilogue it writes fp32 partials as gemm_kernel does.
 //   * 256x256, 8 waves (128x64 wave tiles), 2 stages: large M (batch 64);
 //   * 128x128, 8 waves and 64x128, 4 waves (32x64 wave tiles), 3 stages
 //     (2 for 128x128 grids of several rounds): medium M (batch 1), where the

@@ -103,24 +103,29 @@ __device__ __forceinline__ float wave_sum(float x) {
 
 // Pulls part of [p, p + bytes) into the chip's memory-side cache ahead of
 // the kernel that reads it next (the weights of the next GEMM, which would
-// otherwise come cold from HBM): thread t of the grid loads the 16-byte
-// pieces t, t + n, .. (NPF of them, n = the grid's threads) at its kernel's
-// start and discards them at the end, so the loads overlap the kernel's own
-// work.  Reads only inside the buffer; p == nullptr loads nothing.
-template <int NPF>
+// otherwise come cold from HBM): thread t of the grid (NT threads per
+// block) loads the 16-byte pieces t, t + n, .. (NPF of them, n = the grid's
+// threads) at its kernel's start and discards them at the end.  The loads
+// are unconditional: a piece index past the buffer is clamped to its last
+// piece, and with p == nullptr every load reads `fallback` (any readable
+// 16-byte location, e.g. one of the kernel's own inputs).  A conditional
+// load would make the compiler's memory-counter waits for the kernel's own
+// loads (issued before these) also wait for the prefetch.
+template <int NPF, int NT>
 struct Prefetch {
   u32x4 v[NPF];
-  __device__ __forceinline__ void issue(const void* p, size_t bytes) {
-    const size_t n = (size_t)gridDim.x * gridDim.y * gridDim.z * blockDim.x;
+  __device__ __forceinline__ void issue(const void* p, size_t bytes, const void* fallback) {
+    const size_t n = (size_t)gridDim.x * gridDim.y * gridDim.z * NT;
     const size_t t =
-        (((size_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x) * blockDim.x +
+        (((size_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x) * NT +
         threadIdx.x;
-    const u32x4* q = static_cast<const u32x4*>(p);
-    const size_t np = p ? bytes / 16 : 0;
+    const bool on = p != nullptr && bytes >= 16;
+    const u32x4* q = static_cast<const u32x4*>(on ? p : fallback);
+    const size_t last = on ? bytes / 16 - 1 : 0;
 #pragma unroll
     for (int i = 0; i < NPF; ++i) {
       const size_t k = t + (size_t)i * n;
-      v[i] = k < np ? q[k] : u32x4{0u, 0u, 0u, 0u};
+      v[i] = q[k < last ? k : last];
     }
   }
   __device__ __forceinline__ void retire() const {
@@ -156,7 +161,8 @@ struct GemmPlan {
 GemmPlan plan_gemm(int M, int N, int K, bool bf16);
 
 // Split-K scratch shared by every GEMM of a handle (launches are stream
-// ordered): fp32 partial tiles.
+// ordered): partial tiles, fp32, or bf16 for the direct-to-LDS kernel with
+// no epilogue (see gemm_partials).
 struct GemmWork {
   float* ws = nullptr;
 };

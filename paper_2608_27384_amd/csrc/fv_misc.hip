@@ -210,8 +210,34 @@ __global__ __launch_bounds__(256) void embed_adarms_rows_kernel(
 // --------------------------------------- gated residual + next FiLM RMSNorm
 // One block per row: h[row] += gate[chunk] * sum_z part[z][row] (split order,
 // fp32 sums of the partials, which are stored as P), then (norm_off >= 0)
-// u[row] = rmsnorm(h) (1 + scale) + shift.
-template <typename T, typename P>
+// u[row] = rmsnorm(h) (1 + scale) + shift.  Thread t owns columns
+// 4t + 1024 q (q < NQ).  Every load of the block's row is issued before any
+// is used, with no condition on the loads themselves: the split index is
+// clamped to ks - 1 (the KSM slots past ks re-read split ks - 1 and are
+// dropped from the sum) and the column to W - 4 (dropped likewise), so the
+// compiler does not wait for each load on its own.  The prefetch of the next
+// GEMM's weights is issued after them: the in-order memory counter then
+// never makes this kernel's own loads wait behind it.
+template <typename P> struct RawPart;
+template <> struct RawPart<bf16_t> {
+  typedef u32x2 type;  // four bf16
+  __device__ static __forceinline__ type load(const bf16_t* p) {
+    return *reinterpret_cast<const u32x2*>(p);
+  }
+  __device__ static __forceinline__ f32x4 unpack(type v) {
+    return f32x4{__uint_as_float(v[0] << 16), __uint_as_float(v[0] & 0xffff0000u),
+                 __uint_as_float(v[1] << 16), __uint_as_float(v[1] & 0xffff0000u)};
+  }
+};
+template <> struct RawPart<float> {
+  typedef f32x4 type;
+  __device__ static __forceinline__ type load(const float* p) {
+    return *reinterpret_cast<const f32x4*>(p);
+  }
+  __device__ static __forceinline__ f32x4 unpack(type v) { return v; }
+};
+
+template <typename T, typename P, int KSM, int NQ>
 __global__ __launch_bounds__(256) void resid_norm_kernel(const P* __restrict__ part, int ks,
                                                          float* __restrict__ h,
                                                          const float* __restrict__ mod,
@@ -221,55 +247,51 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const P* __restrict__ p
                                                          const void* pf, size_t pf_bytes) {
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x;
-  Prefetch<8> pre;
-  pre.issue(pf, pf_bytes);
   const float* mrow = mod + (size_t)(row / chunk_len) * mod_ld;
-  f32x4 hq[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  const int nrm = norm_off >= 0 ? norm_off : 0;
+  typename RawPart<P>::type pr[NQ][KSM];
+  f32x4 g[NQ], hv[NQ], svq[NQ], bvq[NQ];
+  int col[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    col[q] = 4 * tid + 1024 * q;
+    const int c = min(col[q], W - 4);
+#pragma unroll
+    for (int z = 0; z < KSM; ++z)
+      pr[q][z] = RawPart<P>::load(part + ((size_t)min(z, ks - 1) * rows + row) * W + c);
+    g[q] = *reinterpret_cast<const f32x4*>(mrow + gate_off + c);
+    hv[q] = *reinterpret_cast<const f32x4*>(h + (size_t)row * W + c);
+    svq[q] = *reinterpret_cast<const f32x4*>(mrow + nrm + c);
+    bvq[q] = *reinterpret_cast<const f32x4*>(mrow + nrm + W + c);
+  }
+  Prefetch<8, 256> pre;
+  pre.issue(pf, pf_bytes, h);
   float ss = 0.f;
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int c = 4 * tid + 1024 * q;
-    if (c < W) {
-      f32x4 pz[8];  // every split's load issued before the sum (ks <= 8)
+  for (int q = 0; q < NQ; ++q) {
+    f32x4 acc = RawPart<P>::unpack(pr[q][0]);
 #pragma unroll
-      for (int z = 0; z < 8; ++z)
-        pz[z] = z < ks ? load4_f32(part + ((size_t)z * rows + row) * W + c)
-                       : f32x4{0.f, 0.f, 0.f, 0.f};
-      const f32x4 g = *reinterpret_cast<const f32x4*>(mrow + gate_off + c);
-      f32x4 hv = *reinterpret_cast<const f32x4*>(h + (size_t)row * W + c);
-      f32x4 acc = pz[0];
-#pragma unroll
-      for (int z = 1; z < 8; ++z)
-        if (z < ks) acc += pz[z];
-      hv += g * acc;
-      *reinterpret_cast<f32x4*>(h + (size_t)row * W + c) = hv;
-      hq[q] = hv;
-      ss += hv[0] * hv[0] + hv[1] * hv[1] + hv[2] * hv[2] + hv[3] * hv[3];
+    for (int z = 1; z < KSM; ++z)
+      if (z < ks) acc += RawPart<P>::unpack(pr[q][z]);
+    hv[q] += g[q] * acc;
+    if (col[q] < W) {
+      *reinterpret_cast<f32x4*>(h + (size_t)row * W + col[q]) = hv[q];
+      ss += hv[q][0] * hv[q][0] + hv[q][1] * hv[q][1] + hv[q][2] * hv[q][2] +
+            hv[q][3] * hv[q][3];
     }
   }
   if (norm_off < 0) {
     pre.retire();
     return;
   }
-  f32x4 svq[2], bvq[2];  // the norm's maps are requested before the row sum waits
-#pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int c = 4 * tid + 1024 * q;
-    if (c < W) {
-      svq[q] = *reinterpret_cast<const f32x4*>(mrow + norm_off + c);
-      bvq[q] = *reinterpret_cast<const f32x4*>(mrow + norm_off + W + c);
-    }
-  }
   const float rinv = 1.0f / sqrtf(block_sum_256(ss, red) / (float)W + eps);
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int c = 4 * tid + 1024 * q;
-    if (c < W) {
-      const f32x4 sv = svq[q], bv = bvq[q];
-      const f32x4 hv = hq[q];
-      store4<T>(u + (size_t)row * W + c, hv[0] * rinv * (1.0f + sv[0]) + bv[0],
-                hv[1] * rinv * (1.0f + sv[1]) + bv[1], hv[2] * rinv * (1.0f + sv[2]) + bv[2],
-                hv[3] * rinv * (1.0f + sv[3]) + bv[3]);
+  for (int q = 0; q < NQ; ++q) {
+    if (col[q] < W) {
+      const f32x4 sv = svq[q], bv = bvq[q], x = hv[q];
+      store4<T>(u + (size_t)row * W + col[q], x[0] * rinv * (1.0f + sv[0]) + bv[0],
+                x[1] * rinv * (1.0f + sv[1]) + bv[1], x[2] * rinv * (1.0f + sv[2]) + bv[2],
+                x[3] * rinv * (1.0f + sv[3]) + bv[3]);
     }
   }
   pre.retire();
@@ -707,14 +729,23 @@ template <typename T>
 void launch_resid_norm(const void* part, bool bf16_parts, int ks, float* h, const float* mod,
                        int mod_ld, int gate_off, int norm_off, int chunk_len, float eps, T* u,
                        int rows, int W, const void* pf, size_t pf_bytes, hipStream_t s) {
+  // split slots (power of two >= ks, at most 8) and column groups per thread
+  const int ksm = ks <= 2 ? 2 : ks <= 4 ? 4 : 8;
+  const int nq = W <= 1024 ? 1 : 2;
+  auto go = [&](auto kern, const auto* pp) {
+    hipLaunchKernelGGL(kern, dim3(rows), dim3(256), 0, s, pp, ks, h, mod, mod_ld, gate_off,
+                       norm_off, chunk_len, eps, u, rows, W, pf, pf_bytes);
+  };
+#define FV_RN(P, KSM, NQ) go(resid_norm_kernel<T, P, KSM, NQ>, static_cast<const P*>(part))
+#define FV_RN_Q(P, KSM) (nq == 1 ? FV_RN(P, KSM, 1) : FV_RN(P, KSM, 2))
+#define FV_RN_K(P) (ksm == 2 ? FV_RN_Q(P, 2) : ksm == 4 ? FV_RN_Q(P, 4) : FV_RN_Q(P, 8))
   if (bf16_parts)
-    hipLaunchKernelGGL((resid_norm_kernel<T, bf16_t>), dim3(rows), dim3(256), 0, s,
-                       static_cast<const bf16_t*>(part), ks, h, mod, mod_ld, gate_off, norm_off,
-                       chunk_len, eps, u, rows, W, pf, pf_bytes);
+    FV_RN_K(bf16_t);
   else
-    hipLaunchKernelGGL((resid_norm_kernel<T, float>), dim3(rows), dim3(256), 0, s,
-                       static_cast<const float*>(part), ks, h, mod, mod_ld, gate_off, norm_off,
-                       chunk_len, eps, u, rows, W, pf, pf_bytes);
+    FV_RN_K(float);
+#undef FV_RN_K
+#undef FV_RN_Q
+#undef FV_RN
 }
 
 template <typename T>

@@ -12,6 +12,7 @@
 
 struct fv_handle_s : public fv::Handle {};
 
+
 namespace fv {
 namespace {
 
@@ -394,10 +395,14 @@ void need_prefix(const Handle* h) {
 enum Kind { KIND_STEP = 1, KIND_VELOCITY = 2, KIND_SEQ = 3, KIND_STEP_CACHED = 4,
             KIND_VELOCITY_CACHED = 5 };
 
-// The noise levels a pass uses: the caller's t, or the installed schedule.
-const float* schedule_or(const Handle* h, const float* t) {
+// Batch of the next pass: a staged observation's once the pass switches to it.
+int pending_batch(const Handle* h) { return h->staged_slot >= 0 ? h->staged_batch : h->batch; }
+
+// The noise levels a pass over `batch` streams uses: the caller's t, or the
+// installed schedule.  Checked before anything changes.
+const float* schedule_or(const Handle* h, const float* t, int batch) {
   if (t) return t;
-  if (h->sched_batch != h->batch)
+  if (h->sched_batch != batch)
     fail(FV_ERR_STATE, "t is NULL but no schedule is installed for the active batch "
                        "(call fv_set_schedule)");
   return h->t_cache;
@@ -775,18 +780,20 @@ fv_status fv_decode_step(fv_handle h, float* buffer, const float* t, float* out_
                          void* stream) {
   if (!h) return FV_ERR_INVALID_ARG;
   return guarded(h, [&] {
+    // every check precedes the first side effect (switching to a staged
+    // observation enqueues a wait on the caller's stream)
     need_prefix(h);
     check_ptr(buffer, "buffer");
     if (t) check_ptr(t, "t_per_chunk");
     check_ptr(out_chunk, "out_chunk");
+    const int B = pending_batch(h);
+    const size_t nbuf = (size_t)B * h->T * h->A * 4, nout = (size_t)B * h->C * h->A * 4;
+    if (overlap(buffer, nbuf, out_chunk, nout)) fail(FV_ERR_INVALID_ARG, "buffer and out_chunk overlap");
+    const float* tt = schedule_or(h, t, B);
+    const float* mod = t ? nullptr : h->mod_cache;
     DeviceScope ds(h->device);
     hipStream_t st = static_cast<hipStream_t>(stream);
     activate_staged(h, st);
-    const float* tt = schedule_or(h, t);
-    const float* mod = t ? nullptr : h->mod_cache;
-    const int B = h->batch;
-    const size_t nbuf = (size_t)B * h->T * h->A * 4, nout = (size_t)B * h->C * h->A * 4;
-    if (overlap(buffer, nbuf, out_chunk, nout)) fail(FV_ERR_INVALID_ARG, "buffer and out_chunk overlap");
     run_step(h, t ? KIND_STEP : KIND_STEP_CACHED, buffer, tt, out_chunk, nullptr, 0, st,
              [&](hipStream_t s) {
                forward(h, buffer, tt, B, h->v, h->L, s, mod);
@@ -805,12 +812,14 @@ fv_status fv_velocity(fv_handle h, const float* buffer, const float* t, float* v
     check_ptr(buffer, "buffer");
     if (t) check_ptr(t, "t");
     check_ptr(v_out, "v_out");
+    const int B = pending_batch(h);
+    const size_t nbuf = (size_t)B * h->T * h->A * 4;
+    if (overlap(buffer, nbuf, v_out, nbuf)) fail(FV_ERR_INVALID_ARG, "buffer and v_out overlap");
+    const float* tt = schedule_or(h, t, B);
+    const float* mod = t ? nullptr : h->mod_cache;
     DeviceScope ds(h->device);
     hipStream_t st = static_cast<hipStream_t>(stream);
     activate_staged(h, st);
-    const float* tt = schedule_or(h, t);
-    const float* mod = t ? nullptr : h->mod_cache;
-    const int B = h->batch;
     run_step(h, t ? KIND_VELOCITY : KIND_VELOCITY_CACHED, buffer, tt, v_out, nullptr, 0, st,
              [&](hipStream_t s) { forward(h, buffer, tt, B, v_out, h->L, s, mod); });
     mark_used(h, st);
@@ -846,7 +855,6 @@ fv_status fv_sequential_decode(fv_handle h, const float* noise, int32_t n_steps,
     check_ptr(out_chunk, "out_chunk");
     if (n_steps < 1 || n_steps > 4096) fail(FV_ERR_INVALID_ARG, "n_steps must be in [1, 4096]");
     DeviceScope ds(h->device);
-    activate_staged(h, static_cast<hipStream_t>(stream));
     float* ts = nullptr;
     for (auto& e : h->tscheds)
       if (e.first == n_steps) ts = e.second;
@@ -856,6 +864,7 @@ fv_status fv_sequential_decode(fv_handle h, const float* noise, int32_t n_steps,
       ts = upload_f32(h, tv.data(), tv.size(), false);
       h->tscheds.emplace_back(n_steps, ts);
     }
+    activate_staged(h, static_cast<hipStream_t>(stream));
     const int B = h->batch;
     const size_t n = (size_t)B * h->C * h->A;
     run_step(h, KIND_SEQ, noise, out_chunk, nullptr, nullptr, n_steps,

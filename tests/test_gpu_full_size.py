@@ -1,8 +1,9 @@
 """GPU parity at the benchmark's full sizes, in the configuration bench.py times.
 
 The oracle (fp64) computes sampled outputs: every chunk of one stream for the
-batch-1 workloads, two sampled streams of the 64-stream workload, and one
-emitted chunk of the sequential baseline.  Tolerance: max relative error 1e-2
+batch-1 workloads; for the 64-stream workload every chunk of up to ten
+streams (extreme prefix lengths, every prefix length mod 8) and chunk 0 of all
+64 streams; and one emitted chunk of the sequential baseline.  Tolerance: max relative error 1e-2
 per (stream, chunk) slice in bf16 mode.
 """
 import sys
@@ -38,18 +39,44 @@ def test_velocity_parity_full_size(name):
         case.close()
 
 
-def test_velocity_parity_batched64_sampled_streams():
+def _f64_weights(W):
+    """The weights as fp64 arrays, converted once for many oracle calls."""
+    return {k: (None if a is None else [np.asarray(x, np.float64) for x in a]
+                if isinstance(a, list) else np.asarray(a, np.float64)) for k, a in W.items()}
+
+
+def test_velocity_parity_batched64_all_streams():
+    """Every chunk of the shortest- and longest-prefix streams and of one
+    stream per residue of the prefix length mod 8 (the arena row alignment
+    and the rotary gap depend on it); chunk 0 of all 64 streams.  Chunk 0
+    sees only the prefix and itself (Sec. 3.1 mask), so it equals the
+    velocity of a one-chunk buffer holding it at the same noise level and
+    positions, which the oracle computes cheaply."""
     w = synth.workload("batched64")
     case = Case(w)
     try:
         v = case.gpu_velocity()
         assert np.all(np.isfinite(v))
-        # the shortest-prefix and the longest-prefix stream
-        for b in (int(np.argmin(case.lens)), int(np.argmax(case.lens))):
-            ref = case.oracle_velocity(b)
+        W64 = _f64_weights(case.W)
+        full = [int(np.argmin(case.lens)), int(np.argmax(case.lens))]
+        for r in range(8):
+            hit = [b for b in range(w.batch) if case.lens[b] % 8 == r and b not in full]
+            full += hit[:1]
+        for b in full:
+            ref = oracle.velocity(case.x[b], case.t[b], case.k[:, b], case.v[:, b],
+                                  int(case.lens[b]), W64, w)
             errs = [rel_err(v[b, k], ref[k]) for k in range(w.n_chunks)]
-            _say(f"batched64 stream {b} (P={case.lens[b]}): max rel err {max(errs):.2e}")
+            _say(f"batched64 stream {b} (P={case.lens[b]}, P%8={case.lens[b] % 8}): "
+                 f"max rel err {max(errs):.2e}")
             assert max(errs) < tol(w), (b, errs)
+        worst = 0.0
+        for b in range(w.batch):
+            ref0 = oracle.velocity(case.x[b, :1], case.t[b, :1], case.k[:, b], case.v[:, b],
+                                   int(case.lens[b]), W64, w)[0]
+            e = rel_err(v[b, 0], ref0)
+            worst = max(worst, e)
+            assert e < tol(w), (b, e)
+        _say(f"batched64 chunk 0 of all {w.batch} streams: max rel err {worst:.2e}")
     finally:
         case.close()
 
@@ -106,7 +133,9 @@ def test_decode_steps_lockstep_pi05():
             new, ref_out = oracle.euler_emit_shift(pre[0], case.t[0], v[0], z, np.float32)
             assert np.array_equal(out[0], ref_out)
             assert np.array_equal(post[0, :-1], new[:-1])
-            assert np.max(np.abs(post[0, -1] - z)) <= 1e-6
+            mism = int(np.count_nonzero(post[0, -1] != z))
+            _say(f"pi05 step {s}: refill values differing from the oracle's draw: {mism} of {z.size}")
+            assert mism <= 2 and np.max(np.abs(post[0, -1] - z)) <= 1e-6
             ref_v = oracle.velocity(pre[0], case.t[0], case.k[:, 0], case.v[:, 0],
                                     int(case.lens[0]), case.W, w)
             _, o_out = oracle.euler_emit_shift(pre[0], case.t[0], ref_v, z)

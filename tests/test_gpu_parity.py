@@ -98,7 +98,9 @@ def test_decode_steps_lockstep_tiny():
                 assert rel_err(post[0, k], new[0, k]) < tol(w), (s, k)
             # fresh noise: same Philox draw as the oracle (fp64 Box-Muller on both sides)
             z = oracle.gaussian_chunk(5, s, w.chunk_len, w.action_dim)
-            assert np.max(np.abs(post[0, -1] - z)) <= 1e-6, s
+            mism = int(np.count_nonzero(post[0, -1] != z))
+            print(f"tiny step {s}: refill values differing from the oracle's draw: {mism}")
+            assert mism <= 2 and np.max(np.abs(post[0, -1] - z)) <= 1e-6, s
         assert case.ex.noise_state == (5, 8)
     finally:
         case.close()
@@ -125,6 +127,8 @@ def test_bookkeeping_bit_exact(name):
             assert np.array_equal(post[b, :-1], new[:-1])
             mism += int(np.count_nonzero(post[b, -1] != z))
             assert np.max(np.abs(post[b, -1] - z)) <= 1e-6
+        total = w.batch * w.chunk_len * w.action_dim
+        print(f"{name}: refill values differing from the oracle's draw: {mism} of {total}")
         assert mism <= 2  # fp64 libm ties only
         assert case.ex.noise_state == (123, 2**32 + 8)
     finally:
