@@ -196,6 +196,28 @@ fv_status fv_decode_step(fv_handle h, float *buffer, const float *t_per_chunk, f
                          void *stream);
 
 /*
+ * fv_decode_step_noalloc -- fv_decode_step for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops and
+ * harnesses that forbid hipMalloc.  Same arguments, checks, semantics and
+ * results (bit-identical) as fv_decode_step, but nothing is allocated or
+ * freed: the kernels are launched one by one on `stream` (no graph is
+ * captured or instantiated), and the step's scratch -- the attention
+ * key-split partials and the split-K partial tiles -- lives in a static
+ * device array of FV_NOALLOC_SCRATCH_BYTES (24 MiB) that each GPU the library
+ * runs on holds until the process ends, instead of the handle's own scratch.
+ * A step that needs more (fv_query FV_QUERY_NOALLOC_SCRATCH_BYTES; the
+ * pi0.5-shaped expert needs about 21 MB at batch 1 and more at batch 2 to 8)
+ * returns FV_ERR_INVALID_ARG.  Every call on a GPU shares that GPU's array
+ * and nothing in it needs to start at zero; calls that overlap on one GPU
+ * (from any handle or stream) race.
+ * Errors: as fv_decode_step, plus FV_ERR_INVALID_ARG (scratch too small for
+ * the active batch) and FV_ERR_HIP (the array's address is unavailable).
+ */
+#define FV_NOALLOC_SCRATCH_BYTES (24u << 20)
+fv_status fv_decode_step_noalloc(fv_handle h, float *buffer, const float *t_per_chunk,
+                                 float *out_chunk, void *stream);
+
+/*
  * fv_velocity -- the velocity pass alone (the v_theta of Eq. 1).
  *  buffer dev fp32 [batch][K][C][A] (read only), t dev fp32 [batch][K] (or
  *  NULL: the installed schedule), v_out dev fp32 [batch][K][C][A].  Uses the
@@ -322,11 +344,14 @@ fv_status fv_set_graph_mode(fv_handle h, int32_t enabled);
  *  FV_QUERY_ATTN_SPLITS: number of key ranges the attention splits each
  *    query tile into at batch `batch` (1: no split, no combine kernel);
  *  FV_QUERY_DEVICE_BYTES: device memory the handle holds (weights, prefix
- *    arenas, scratch, workspace), in bytes; `batch` is ignored.
+ *    arenas, scratch, workspace), in bytes; `batch` is ignored;
+ *  FV_QUERY_NOALLOC_SCRATCH_BYTES: static scratch fv_decode_step_noalloc
+ *    needs for a step at batch `batch` (accepted when at most
+ *    FV_NOALLOC_SCRATCH_BYTES).
  * `value` is a host pointer.  Errors: FV_ERR_INVALID_ARG (NULL handle or
  * value, unknown `what`, batch outside 1..max_batch for the split query).
  */
-enum { FV_QUERY_ATTN_SPLITS = 1, FV_QUERY_DEVICE_BYTES = 2 };
+enum { FV_QUERY_ATTN_SPLITS = 1, FV_QUERY_DEVICE_BYTES = 2, FV_QUERY_NOALLOC_SCRATCH_BYTES = 3 };
 fv_status fv_query(fv_handle h, int32_t what, int32_t batch, int64_t *value);
 
 /* fv_destroy -- synchronise the device and free everything the handle owns. */

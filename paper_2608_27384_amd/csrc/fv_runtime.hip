@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstring>
 #include <exception>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -12,6 +13,13 @@
 
 struct fv_handle_s : public fv::Handle {};
 
+// Scratch of fv_decode_step_noalloc: the attention key-split partials and
+// the split-K partial tiles of one step, in a fixed array that every GPU the
+// library runs on holds until the process ends (each GPU its own copy, at
+// its own address).  Host code never uses this name as an address: the
+// per-device address comes from hipGetSymbolAddress (see static_scratch).
+constexpr size_t kStaticScratchBytes = FV_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 
 namespace fv {
 namespace {
@@ -387,6 +395,81 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb) {
   return x < y + nb && y < x + na;
 }
 
+// Device address of `scratch` per device ordinal, looked up once per device
+// (with that device current) when the first handle on it is created.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+hipError_t g_scratch_err[kMaxDevices] = {};
+bool g_scratch_done[kMaxDevices] = {};
+
+void lookup_static_scratch(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_done[dev]) return;
+  void* p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  g_scratch_err[dev] = e;
+  g_scratch_ptr[dev] = e == hipSuccess ? p : nullptr;
+  if (e != hipSuccess) (void)hipGetLastError();
+  g_scratch_done[dev] = true;
+}
+
+void* static_scratch(int dev) {
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (dev < 0 || dev >= kMaxDevices || !g_scratch_done[dev] || !g_scratch_ptr[dev])
+    fail(FV_ERR_HIP, std::string("no static scratch address on this device: ") +
+                         (dev >= 0 && dev < kMaxDevices && g_scratch_done[dev]
+                              ? hipGetErrorString(g_scratch_err[dev])
+                              : "device not set up"));
+  return g_scratch_ptr[dev];
+}
+
+size_t round256(size_t n) { return (n + 255) & ~size_t(255); }
+
+// Scratch one step at `batch` streams needs: attention split partials
+// (element type) and their (max, sum) pairs, and the largest split-K
+// workspace of the step's GEMMs.
+struct StepScratch {
+  size_t part_o = 0, part_ml = 0, ws = 0;
+  size_t total() const { return part_o + part_ml + ws; }
+};
+StepScratch step_scratch(const Handle* h, int B) {
+  StepScratch r;
+  const int s = attn_split(h, B);
+  if (s > 1) {
+    const size_t rows = (size_t)s * B * h->T * h->Hq;
+    r.part_o = round256(rows * h->dh * h->esz);
+    r.part_ml = round256(rows * 2 * 4);
+  }
+  const int W = h->W, rk = B * h->K, rt = B * h->T, qd = h->Hq * h->dh;
+  const GemmPlan ps[] = {plan_gemm(rk, W, W, h->bf16), plan_gemm(rk, h->Nmod, W, h->bf16),
+                         plan_gemm(rt, h->Nqkv, W, h->bf16), plan_gemm(rt, W, qd, h->bf16),
+                         plan_gemm(rt, h->Ngu, W, h->bf16), plan_gemm(rt, W, h->F, h->bf16)};
+  for (const GemmPlan& p : ps) r.ws = std::max(r.ws, round256(p.ws_floats * 4));
+  return r;
+}
+
+// Points the handle's split partials and split-K workspace at caller-given
+// memory for the duration of an eager (uncaptured) pass, then restores them.
+struct ScratchSwap {
+  Handle* h;
+  float* ws;
+  void* part_o;
+  float* part_ml;
+  ScratchSwap(Handle* hh, unsigned char* base, const StepScratch& sz)
+      : h(hh), ws(hh->gw.ws), part_o(hh->part_o), part_ml(hh->part_ml) {
+    h->part_o = base;
+    h->part_ml = reinterpret_cast<float*>(base + sz.part_o);
+    h->gw.ws = reinterpret_cast<float*>(base + sz.part_o + sz.part_ml);
+  }
+  ~ScratchSwap() {
+    h->gw.ws = ws;
+    h->part_o = part_o;
+    h->part_ml = part_ml;
+  }
+};
+
 void need_prefix(const Handle* h) {
   if (!h->prefix_set && h->staged_slot < 0)
     fail(FV_ERR_STATE, "no observation prefix: call fv_set_prefix first");
@@ -521,6 +604,7 @@ fv_status fv_create(const fv_weights* w, const fv_cfg* cfg, fv_handle* out) {
     }
 
     FV_HIP(hipGetDevice(&H.device));
+    lookup_static_scratch(H.device);
     if (H.bf16) {
       FV_HIP(gemm_prepare());
       FV_HIP(attention_prepare());
@@ -804,6 +888,42 @@ fv_status fv_decode_step(fv_handle h, float* buffer, const float* t, float* out_
   });
 }
 
+fv_status fv_decode_step_noalloc(fv_handle h, float* buffer, const float* t, float* out_chunk,
+                                 void* stream) {
+  if (!h) return FV_ERR_INVALID_ARG;
+  return guarded(h, [&] {
+    need_prefix(h);
+    check_ptr(buffer, "buffer");
+    if (t) check_ptr(t, "t_per_chunk");
+    check_ptr(out_chunk, "out_chunk");
+    const int B = pending_batch(h);
+    const size_t nbuf = (size_t)B * h->T * h->A * 4, nout = (size_t)B * h->C * h->A * 4;
+    if (overlap(buffer, nbuf, out_chunk, nout)) fail(FV_ERR_INVALID_ARG, "buffer and out_chunk overlap");
+    const float* tt = schedule_or(h, t, B);
+    const float* mod = t ? nullptr : h->mod_cache;
+    const StepScratch need = step_scratch(h, B);
+    if (need.total() > kStaticScratchBytes)
+      fail(FV_ERR_INVALID_ARG, "a step at batch " + std::to_string(B) + " needs " +
+                                   std::to_string(need.total()) +
+                                   " bytes of scratch; the static scratch holds " +
+                                   std::to_string(kStaticScratchBytes) +
+                                   " (use fv_decode_step)");
+    DeviceScope ds(h->device);
+    unsigned char* base = static_cast<unsigned char*>(static_scratch(h->device));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    activate_staged(h, st);
+    {
+      ScratchSwap sw(h, base, need);
+      (void)hipGetLastError();
+      forward(h, buffer, tt, B, h->v, h->L, st, mod);
+      launch_euler_shift(buffer, tt, h->v, out_chunk, h->d_noise, h->d_ticket, h->d_valid, B,
+                         h->K, h->C * h->A, st);
+      check_launch();
+    }
+    mark_used(h, st);
+  });
+}
+
 fv_status fv_velocity(fv_handle h, const float* buffer, const float* t, float* v_out,
                       void* stream) {
   if (!h) return FV_ERR_INVALID_ARG;
@@ -1042,6 +1162,10 @@ fv_status fv_query(fv_handle h, int32_t what, int32_t batch, int64_t* value) {
         break;
       case FV_QUERY_DEVICE_BYTES:
         *value = (int64_t)h->device_bytes;
+        break;
+      case FV_QUERY_NOALLOC_SCRATCH_BYTES:
+        if (batch < 1 || batch > h->Bmax) fail(FV_ERR_INVALID_ARG, "batch outside 1..max_batch");
+        *value = (int64_t)step_scratch(h, batch).total();
         break;
       default:
         fail(FV_ERR_INVALID_ARG, "unknown query");

@@ -19,7 +19,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libflashvla
 
 FV_OK, FV_ERR_INVALID_ARG, FV_ERR_STATE, FV_ERR_OOM, FV_ERR_HIP, FV_ERR_INTERNAL = range(6)
 FV_BF16, FV_FP32 = 0, 1
-FV_QUERY_ATTN_SPLITS, FV_QUERY_DEVICE_BYTES = 1, 2
+FV_QUERY_ATTN_SPLITS, FV_QUERY_DEVICE_BYTES, FV_QUERY_NOALLOC_SCRATCH_BYTES = 1, 2, 3
+FV_NOALLOC_SCRATCH_BYTES = 24 << 20
 FV_MASK_CHUNK_CAUSAL, FV_MASK_ISOLATED, FV_MASK_BIDIRECTIONAL = 0, 1, 2
 MASK_MODES = {"causal": FV_MASK_CHUNK_CAUSAL, "isolated": FV_MASK_ISOLATED,
               "bidirectional": FV_MASK_BIDIRECTIONAL}
@@ -30,6 +31,7 @@ EXPORTED = (
     "fv_destroy", "fv_status_string", "fv_last_error", "fv_abi_version", "fv_debug_forward",
     "fv_debug_stage", "fv_query", "fv_set_mask_mode", "fv_set_schedule", "fv_cold_start",
     "fv_get_valid_slots", "fv_set_valid_slots", "fv_multibuffer_velocity", "fv_set_prefix_async",
+    "fv_decode_step_noalloc",
 )
 
 
@@ -68,6 +70,7 @@ def lib() -> ctypes.CDLL:
             "fv_create": ([POINTER(FvWeights), POINTER(FvCfg), POINTER(c_void_p)], S),
             "fv_set_prefix": ([H, c_void_p, c_void_p, POINTER(c_int32), c_int32, c_int32, c_void_p], S),
             "fv_decode_step": ([H, c_void_p, c_void_p, c_void_p, c_void_p], S),
+            "fv_decode_step_noalloc": ([H, c_void_p, c_void_p, c_void_p, c_void_p], S),
             "fv_velocity": ([H, c_void_p, c_void_p, c_void_p, c_void_p], S),
             "fv_euler_shift": ([H, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p], S),
             "fv_sequential_decode": ([H, c_void_p, c_int32, c_void_p, c_void_p], S),
@@ -185,6 +188,11 @@ def fv_decode_step(h, buffer, t, out_chunk, stream=None) -> None:
            "fv_decode_step")
 
 
+def fv_decode_step_noalloc(h, buffer, t, out_chunk, stream=None) -> None:
+    _check(h, lib().fv_decode_step_noalloc(h, _ptr(buffer), _ptr(t), _ptr(out_chunk),
+                                           _stream(stream)), "fv_decode_step_noalloc")
+
+
 def fv_velocity(h, buffer, t, v_out, stream=None) -> None:
     _check(h, lib().fv_velocity(h, _ptr(buffer), _ptr(t), _ptr(v_out), _stream(stream)),
            "fv_velocity")
@@ -287,6 +295,13 @@ class Expert:
 
     def decode_step(self, buffer, t, out_chunk, stream=None):
         fv_decode_step(self.handle, buffer, t, out_chunk, stream)
+
+    def decode_step_noalloc(self, buffer, t, out_chunk, stream=None):
+        fv_decode_step_noalloc(self.handle, buffer, t, out_chunk, stream)
+
+    def noalloc_scratch_bytes(self, batch=None) -> int:
+        return fv_query(self.handle, FV_QUERY_NOALLOC_SCRATCH_BYTES,
+                        self.batch if batch is None else batch)
 
     def velocity(self, buffer, t, v_out, stream=None):
         fv_velocity(self.handle, buffer, t, v_out, stream)
