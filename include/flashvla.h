@@ -347,11 +347,15 @@ fv_status fv_set_graph_mode(fv_handle h, int32_t enabled);
  *    arenas, scratch, workspace), in bytes; `batch` is ignored;
  *  FV_QUERY_NOALLOC_SCRATCH_BYTES: static scratch fv_decode_step_noalloc
  *    needs for a step at batch `batch` (accepted when at most
- *    FV_NOALLOC_SCRATCH_BYTES).
+ *    FV_NOALLOC_SCRATCH_BYTES);
+ *  FV_QUERY_OUT_PROJ_SPLITS: split-K factor of the output projection at batch
+ *    `batch` (1: unsplit, the gated residual runs in the GEMM's epilogue;
+ *    more: split partials reduced with the residual and the next norm).
  * `value` is a host pointer.  Errors: FV_ERR_INVALID_ARG (NULL handle or
  * value, unknown `what`, batch outside 1..max_batch for the split query).
  */
-enum { FV_QUERY_ATTN_SPLITS = 1, FV_QUERY_DEVICE_BYTES = 2, FV_QUERY_NOALLOC_SCRATCH_BYTES = 3 };
+enum { FV_QUERY_ATTN_SPLITS = 1, FV_QUERY_DEVICE_BYTES = 2, FV_QUERY_NOALLOC_SCRATCH_BYTES = 3,
+       FV_QUERY_OUT_PROJ_SPLITS = 4 };
 fv_status fv_query(fv_handle h, int32_t what, int32_t batch, int64_t *value);
 
 /* fv_destroy -- synchronise the device and free everything the handle owns. */
@@ -383,20 +387,30 @@ fv_status fv_debug_forward(fv_handle h, const float *buffer, const float *t,
  * fv_debug_stage -- measurement aid: re-launches one kernel stage of the most
  * recent velocity pass (fv_velocity, fv_decode_step or fv_debug_forward with
  * the same batch) `reps` times on `stream`, reading the activations that pass
- * left in the handle's scratch memory.  Stages 0-5 rewrite scratch memory
- * only and give the same result on every repetition; stages 6 and 7 add into
- * the residual stream on every repetition (timing aid only: run a velocity
- * pass again before reading results).
+ * left in the handle's scratch memory.  `layer` selects the layer's weights
+ * and arena; -1 makes repetition r use layer r mod L, as a step walks the
+ * layers.  In graph mode (the default) the reps launches are captured once
+ * into a HIP graph and replayed, so each launch is dispatched as inside a
+ * step.  Stages 0-5 rewrite scratch memory only and give the same result on
+ * every repetition; stages 6-11 add into the residual stream or rewrite the
+ * normalised activations (timing aid only: run a velocity pass again before
+ * reading results).
  *  stage 0: FiLM maps (cond -> every norm's [scale | shift | gate]);
- *  stage 1: packed QKV GEMM + rotary + K/V arena write of layer `layer`;
- *  stage 2: chunk-causal attention of layer `layer` (both kernels);
- *  stage 3: packed gate/up GEMM + GeGLU (or GELU) of layer `layer`;
+ *  stage 1: packed QKV GEMM + rotary + K/V arena write;
+ *  stage 2: chunk-causal attention (both kernels);
+ *  stage 3: packed gate/up GEMM + GeGLU (or GELU);
  *  stage 4: attention score/value kernel alone (per-split partials);
  *  stage 5: attention split combine alone (no launch when nothing is split);
  *  stage 6: output projection + gated residual + next FiLM RMSNorm;
- *  stage 7: down projection + gated residual + next FiLM RMSNorm.
- * Errors: FV_ERR_STATE (no prefix), FV_ERR_INVALID_ARG (stage, layer or reps
- * out of range: stage 0..7, reps 1..100000).
+ *  stage 7: down projection + gated residual + next FiLM RMSNorm;
+ *  stage 8: output projection GEMM alone (its split-K partials, or the GEMM
+ *           with the gated residual in its epilogue when k is not split);
+ *  stage 9: down projection GEMM alone (likewise);
+ *  stage 10: the kernel after the output projection alone (split-K reduction
+ *           + gated residual + FiLM norm, or the FiLM norm);
+ *  stage 11: the kernel after the down projection alone (likewise).
+ * Errors: FV_ERR_STATE (no prefix, or a staged observation pending),
+ * FV_ERR_INVALID_ARG (stage 0..11, layer -1..L-1, reps 1..100000).
  */
 fv_status fv_debug_stage(fv_handle h, int32_t stage, int32_t layer, int32_t reps, void *stream);
 

@@ -1035,6 +1035,12 @@ GemmPlan plan_gemm(int M, int N, int K, bool bf16) {
 }
 
 
+// The direct-to-LDS tiles (every bf16 tile but 32x128) store bf16 partials.
+bool gemm_partials_bf16(const GemmPlan& p, bool bf16) {
+  return bf16 && p.ks > 1 &&
+         (p.tile == T256x256big || p.tile == T128x128w8 || p.tile == T64x128w4);
+}
+
 template <typename T>
 int gemm_partials(const T* A, const T* Bt, int M, int N, int K, const GemmWork& w,
                   hipStream_t s, bool* bf16_parts) {

@@ -203,6 +203,8 @@ void gemm_gelu(const T* A, const T* Bt, T* out, int M, int N, int K, const GemmW
 // Raises the dynamic LDS limit of the large-M GEMM kernels (call once per
 // device before the first GEMM launch).
 hipError_t gemm_prepare();
+// Whether gemm_partials stores the partials of plan p as bf16.
+bool gemm_partials_bf16(const GemmPlan& p, bool bf16);
 // Split-K GEMM that only writes its partials [KS][M][N] to w.ws; returns KS,
 // or 1 (nothing launched) when the plan does not split k.  *bf16_parts: the
 // partials are bf16 (the direct-to-LDS tiles), else fp32.

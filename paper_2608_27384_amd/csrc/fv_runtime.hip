@@ -182,12 +182,13 @@ void resid_block(Handle* h, const float* mod, const T* A, const T* Bt, int K, in
   const int W = h->W;
   bool bf16_parts = false;
   const int ks = gemm_partials<T>(A, Bt, rowsT, W, K, h->gw, s, &bf16_parts);
+  if (ks <= 1)
+    gemm_gated_resid<T>(A, Bt, h->hres, mod, h->Nmod, gate_off, h->C, rowsT, W, K, h->gw, s);
   if (ks > 1) {
     launch_resid_norm<T>(h->gw.ws, bf16_parts, ks, h->hres, mod, h->Nmod, gate_off, norm_off,
                          h->C, h->cfg.rms_eps, (T*)h->u, rowsT, W,
                          FV_PREFETCH ? next_w : nullptr, next_bytes, s);
   } else {
-    gemm_gated_resid<T>(A, Bt, h->hres, mod, h->Nmod, gate_off, h->C, rowsT, W, K, h->gw, s);
     if (norm_off >= 0)
       launch_adarms<T>(h->hres, mod, h->Nmod, norm_off, h->C, h->cfg.rms_eps, (T*)h->u, rowsT,
                        W, s);
@@ -240,9 +241,9 @@ void enqueue_forward(Handle* h, const float* buffer, const float* t, int B, floa
     gemm_qkv<T>((T*)h->u, (const T*)h->wqkv[l], qa, rowsT, h->Nqkv, W, h->gw, s);
     // each kernel ahead of a GEMM pulls that GEMM's weights into the
     // memory-side cache while it runs
-    launch_attention<T>(attn_args(h, kar, var, B, n_split, h->wo[l],
-                                  (size_t)W * h->Hq * h->dh * h->esz),
-                        s);
+    const AttnArgs aa = attn_args(h, kar, var, B, n_split, h->wo[l],
+                                  (size_t)W * h->Hq * h->dh * h->esz);
+    launch_attention<T>(aa, s);
     resid_block<T>(h, mod, (const T*)h->o, (const T*)h->wo[l], h->Hq * h->dh,
                    n_attn * 3 * W + 2 * W, n_mlp * 3 * W, rowsT, s, h->wgu[l],
                    (size_t)h->Ngu * W * h->esz);
@@ -260,12 +261,62 @@ void enqueue_forward(Handle* h, const float* buffer, const float* t, int B, floa
                  v_out, rowsT, W, h->A, s);
 }
 
+// One projection GEMM with the gated residual, alone: the split-K partials
+// (when k is split) or the GEMM with the residual in its epilogue.
+template <typename T>
+void proj_gemm_only(Handle* h, const T* A, const T* Bt, int K, int gate_off, int rowsT,
+                    hipStream_t s) {
+  bool bf16_parts = false;
+  if (gemm_partials<T>(A, Bt, rowsT, h->W, K, h->gw, s, &bf16_parts) <= 1)
+    gemm_gated_resid<T>(A, Bt, h->hres, h->mod, h->Nmod, gate_off, h->C, rowsT, h->W, K, h->gw,
+                        s);
+}
+
+// The FiLM norm that follows a projection, alone: the split-K reduction with
+// the gated residual and the norm (when k is split), or the plain norm.
+// As in a step, the reduction pulls the next GEMM's weights [pf, pf + bytes)
+// into the memory-side cache meanwhile.
+template <typename T>
+void proj_norm_only(Handle* h, int K, int gate_off, int norm_off, int rowsT, hipStream_t s,
+                    const void* pf, size_t pf_bytes) {
+  const GemmPlan p = plan_gemm(rowsT, h->W, K, h->bf16);
+  if (p.ks > 1)
+    launch_resid_norm<T>(h->gw.ws, gemm_partials_bf16(p, h->bf16), p.ks, h->hres, h->mod, h->Nmod,
+                         gate_off, norm_off, h->C, h->cfg.rms_eps, (T*)h->u, rowsT, h->W,
+                         FV_PREFETCH ? pf : nullptr, pf_bytes, s);
+  else if (norm_off >= 0)
+    launch_adarms<T>(h->hres, h->mod, h->Nmod, norm_off, h->C, h->cfg.rms_eps, (T*)h->u, rowsT,
+                     h->W, s);
+}
+
 template <typename T>
 void run_stage(Handle* h, int stage, int l, hipStream_t s) {
   const int B = h->batch, W = h->W, rowsK = B * h->K, rowsT = B * h->T;
   const size_t layer_elems = (size_t)h->Bmax * h->Hkv * h->S * h->dh;
   T* kar = (T*)h->karena + l * layer_elems;
   T* var = (T*)h->vtarena + l * layer_elems;
+  const int n_attn = 2 * l, n_mlp = 2 * l + 1;
+  switch (stage) {
+    case 8:
+      proj_gemm_only<T>(h, (const T*)h->o, (const T*)h->wo[l], h->Hq * h->dh,
+                        n_attn * 3 * W + 2 * W, rowsT, s);
+      return;
+    case 9:
+      proj_gemm_only<T>(h, (const T*)h->m, (const T*)h->wd[l], h->F, n_mlp * 3 * W + 2 * W,
+                        rowsT, s);
+      return;
+    case 10:
+      proj_norm_only<T>(h, h->Hq * h->dh, n_attn * 3 * W + 2 * W, n_mlp * 3 * W, rowsT, s,
+                        h->wgu[l], (size_t)h->Ngu * W * h->esz);
+      return;
+    case 11:
+      proj_norm_only<T>(h, h->F, n_mlp * 3 * W + 2 * W,
+                        l + 1 < h->L ? 2 * (l + 1) * 3 * W : -1, rowsT, s,
+                        l + 1 < h->L ? h->wqkv[l + 1] : nullptr, (size_t)h->Nqkv * W * h->esz);
+      return;
+    default:
+      break;
+  }
   switch (stage) {
     case 0:
       gemm_bias_f32<T>((T*)h->cond, (T*)h->w_mod, h->b_mod, h->mod, rowsK, h->Nmod, W, h->gw, s);
@@ -279,18 +330,17 @@ void run_stage(Handle* h, int stage, int l, hipStream_t s) {
     case 2:
     case 4:
     case 5: {
-      launch_attention<T>(attn_args(h, kar, var, B, attn_split(h, B)), s,
-                          stage == 2 ? 3 : stage == 4 ? 1 : 2);
+      launch_attention<T>(attn_args(h, kar, var, B, attn_split(h, B), h->wo[l],
+                                    (size_t)W * h->Hq * h->dh * h->esz),
+                          s, stage == 2 ? 3 : stage == 4 ? 1 : 2);
       break;
     }
     case 6: {
-      const int n_attn = 2 * l, n_mlp = 2 * l + 1;
       resid_block<T>(h, h->mod, (const T*)h->o, (const T*)h->wo[l], h->Hq * h->dh,
                      n_attn * 3 * W + 2 * W, n_mlp * 3 * W, rowsT, s);
       break;
     }
     case 7: {
-      const int n_mlp = 2 * l + 1;
       const int next_norm = l + 1 < h->L ? 2 * (l + 1) * 3 * W : -1;
       resid_block<T>(h, h->mod, (const T*)h->m, (const T*)h->wd[l], h->F, n_mlp * 3 * W + 2 * W,
                      next_norm, rowsT, s);
@@ -476,7 +526,7 @@ void need_prefix(const Handle* h) {
 }
 
 enum Kind { KIND_STEP = 1, KIND_VELOCITY = 2, KIND_SEQ = 3, KIND_STEP_CACHED = 4,
-            KIND_VELOCITY_CACHED = 5 };
+            KIND_VELOCITY_CACHED = 5, KIND_STAGE = 6 };
 
 // Batch of the next pass: a staged observation's once the pass switches to it.
 int pending_batch(const Handle* h) { return h->staged_slot >= 0 ? h->staged_batch : h->batch; }
@@ -1163,6 +1213,10 @@ fv_status fv_query(fv_handle h, int32_t what, int32_t batch, int64_t* value) {
       case FV_QUERY_DEVICE_BYTES:
         *value = (int64_t)h->device_bytes;
         break;
+      case FV_QUERY_OUT_PROJ_SPLITS:
+        if (batch < 1 || batch > h->Bmax) fail(FV_ERR_INVALID_ARG, "batch outside 1..max_batch");
+        *value = plan_gemm(batch * h->T, h->W, h->Hq * h->dh, h->bf16).ks;
+        break;
       case FV_QUERY_NOALLOC_SCRATCH_BYTES:
         if (batch < 1 || batch > h->Bmax) fail(FV_ERR_INVALID_ARG, "batch outside 1..max_batch");
         *value = (int64_t)step_scratch(h, batch).total();
@@ -1199,19 +1253,23 @@ fv_status fv_debug_stage(fv_handle h, int32_t stage, int32_t layer, int32_t reps
   if (!h) return FV_ERR_INVALID_ARG;
   return guarded(h, [&] {
     need_prefix(h);
-    if (stage < 0 || stage > 7) fail(FV_ERR_INVALID_ARG, "stage must be 0..7");
-    if (layer < 0 || layer >= h->L) fail(FV_ERR_INVALID_ARG, "layer out of range");
+    if (stage < 0 || stage > 11) fail(FV_ERR_INVALID_ARG, "stage must be 0..11");
+    if (layer < -1 || layer >= h->L) fail(FV_ERR_INVALID_ARG, "layer out of range");
     if (reps < 1 || reps > 100000) fail(FV_ERR_INVALID_ARG, "reps must be 1..100000");
+    if (h->staged_slot >= 0) fail(FV_ERR_STATE, "a staged observation is pending");
     DeviceScope ds(h->device);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    (void)hipGetLastError();
-    for (int r = 0; r < reps; ++r) {
-      if (h->bf16)
-        run_stage<bf16_t>(h, stage, layer, s);
-      else
-        run_stage<float>(h, stage, layer, s);
-    }
-    check_launch();
+    // layer -1: repetition r runs layer r mod L, as the step walks the layers
+    run_step(h, KIND_STAGE, nullptr, nullptr, nullptr, nullptr,
+             (stage + 16 * (layer + 1)) + 4096 * reps, s, [&](hipStream_t st) {
+               for (int r = 0; r < reps; ++r) {
+                 const int l = layer >= 0 ? layer : r % h->L;
+                 if (h->bf16)
+                   run_stage<bf16_t>(h, stage, l, st);
+                 else
+                   run_stage<float>(h, stage, l, st);
+               }
+             });
     mark_used(h, s);
   });
 }

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libflashvla
 FV_OK, FV_ERR_INVALID_ARG, FV_ERR_STATE, FV_ERR_OOM, FV_ERR_HIP, FV_ERR_INTERNAL = range(6)
 FV_BF16, FV_FP32 = 0, 1
 FV_QUERY_ATTN_SPLITS, FV_QUERY_DEVICE_BYTES, FV_QUERY_NOALLOC_SCRATCH_BYTES = 1, 2, 3
+FV_QUERY_OUT_PROJ_SPLITS = 4
 FV_NOALLOC_SCRATCH_BYTES = 24 << 20
 FV_MASK_CHUNK_CAUSAL, FV_MASK_ISOLATED, FV_MASK_BIDIRECTIONAL = 0, 1, 2
 MASK_MODES = {"causal": FV_MASK_CHUNK_CAUSAL, "isolated": FV_MASK_ISOLATED,
@@ -348,6 +349,10 @@ class Expert:
 
     def attn_split(self, batch=None) -> int:
         return fv_query(self.handle, FV_QUERY_ATTN_SPLITS, self.batch if batch is None else batch)
+
+    def out_proj_splits(self, batch=None) -> int:
+        return fv_query(self.handle, FV_QUERY_OUT_PROJ_SPLITS,
+                        self.batch if batch is None else batch)
 
     def device_bytes(self) -> int:
         return fv_query(self.handle, FV_QUERY_DEVICE_BYTES)
