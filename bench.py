@@ -473,8 +473,12 @@ def _observations(w, n, seed0=200):
     return obs
 
 
-def measure_async_pipeline(w, steps=60, warmup=6, hz=30.0, horizon=16, delays=(0, 1, 2),
-                           segments=8, inp=None):
+LOOP_MODES = ("serialized", "pipelined_same_stream", "pipelined_copy_stream")
+
+
+def measure_async_pipeline(w, steps=60, warmup=6, hz=30.0, horizons=(16, 5, 2),
+                           delays=(0, 1, 2), segments=8, inp=None, modes=LOOP_MODES,
+                           timeline=True):
     """Asynchronous execution (Sec. 4.2) and reaction speed (Sec. 4.3).
 
     1. Back-to-back control loop (the highest control rate the GPU allows):
@@ -488,7 +492,10 @@ def measure_async_pipeline(w, steps=60, warmup=6, hz=30.0, horizon=16, delays=(0
          the install of observation i+1 runs concurrently with step i.
        Wall clock per control step, host calls included.
     2. The paper's timeline with a synthetic executor at `hz`: each segment
-       executes E = `horizon` actions of the emitted chunk; the inference for
+       executes E actions of the emitted chunk (E in `horizons`: 16 is the
+       execution horizon of the paper's RoboTwin and real-robot runs, 5 its
+       LIBERO replanning interval, 2 the segment its reaction-speed figures
+       imply: TTR - TTFA = 33 ms = 0.5 * 2 / 30 Hz); the inference for
        the next segment is launched after E - d actions and its chunk is
        executed after the current segment ends (d = 0: synchronous, the
        robot waits for it).  The executor is simulated on the host clock
@@ -503,9 +510,9 @@ def measure_async_pipeline(w, steps=60, warmup=6, hz=30.0, horizon=16, delays=(0
     inp = inp or Inputs(w)
     obs = _observations(w, 2)
     res = {"workload": w.name, "batch": w.batch, "steps": steps, "executor_hz": hz,
-           "horizon_E": horizon}
+           "horizons_E": list(horizons)}
     loop = {}
-    for mode in ("serialized", "pipelined_same_stream", "pipelined_copy_stream"):
+    for mode in modes:
         ex = Expert(inp.W, w, w.batch, w.max_prefix, noise_seed=w.noise_seed)
         try:
             xd = torch.from_numpy(inp.x.copy()).cuda()
@@ -535,6 +542,8 @@ def measure_async_pipeline(w, steps=60, warmup=6, hz=30.0, horizon=16, delays=(0
         finally:
             ex.close()
     res["control_loop"] = loop
+    if not timeline:
+        return res
 
     # timeline of Sec. 4.2 with a synthetic executor
     ex = Expert(inp.W, w, w.batch, w.max_prefix, noise_seed=w.noise_seed)
@@ -551,7 +560,7 @@ def measure_async_pipeline(w, steps=60, warmup=6, hz=30.0, horizon=16, delays=(0
         torch.cuda.synchronize()
         period = 1.0 / hz
         timeline = {}
-        for d in delays:
+        for horizon, d in [(E, d) for E in horizons for d in delays if d < E]:
             lat, stall = [], []
             t_seg = time.perf_counter()
             for n in range(segments):
@@ -571,7 +580,7 @@ def measure_async_pipeline(w, steps=60, warmup=6, hz=30.0, horizon=16, delays=(0
                 stall.append(st)
                 t_seg = seg_end + st
             ttfa = pct(lat, 50) * 1e3
-            timeline[f"d{d}"] = {"delay_actions": d,
+            timeline[f"E{horizon}_d{d}"] = {"horizon_actions": horizon, "delay_actions": d,
                                  "ttfa_ms_p50": ttfa, "ttfa_ms_p99": pct(lat, 99) * 1e3,
                                  "stall_ms_per_segment": 1e3 * float(np.mean(stall)),
                                  "actions_per_s": horizon / (horizon * period +
@@ -701,7 +710,7 @@ def _cpu_runs(workloads, inputs, model, threads):
             t0 = time.perf_counter()
             oracle.sequential_decode(x[:, 0], w.seq_steps, k, v, lens, W, w, dtype=np.float32)
             sec = (time.perf_counter() - t0) / n
-            unit_note = f"{w.seq_steps} Euler passes of one chunk per emitted chunk"
+            unit_note = f"emitted chunk(s) of {w.seq_steps} Euler passes each"
         else:
             xx = x
             for i in range(warm):
@@ -749,6 +758,9 @@ def main():
     ap.add_argument("--no-others", action="store_true")
     ap.add_argument("--no-stages", action="store_true",
                     help="skip the per-kernel stage timing (decode steps only)")
+    ap.add_argument("--control-loop", default=None, choices=LOOP_MODES,
+                    help="only the back-to-back control loop of the asynchronous pipeline in "
+                         "this mode (for a kernel trace); prints its JSON")
     ap.add_argument("--pmc-driver", default=None, metavar="WHAT",
                     help="counter-run driver: 'step' (decode steps) or a comma-separated list "
                          "of stages (" + "|".join(DEBUG_STAGES) + "), then the 256 MiB "
@@ -766,6 +778,10 @@ def main():
     w = synth.workload(args.workload)
     if args.pmc_driver:
         pmc_driver(w, args.pmc_driver)
+        return
+    if args.control_loop:
+        print(json.dumps(measure_async_pipeline(w, steps=args.steps, warmup=args.warmup,
+                                                modes=(args.control_loop,), timeline=False)))
         return
     inputs = {w.name: Inputs(w)}
     main_res = measure_streaming(w, args.steps, args.warmup, with_roofline=not args.no_stages,
