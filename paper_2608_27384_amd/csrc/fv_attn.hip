@@ -914,23 +914,29 @@ __global__ __launch_bounds__(256) void attn_combine(const T* __restrict__ part_o
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= R) return;
-  // every load of the row is issued before any is used (n_split <= 8)
+  // every load of the row is issued before any is used (n_split <= 8), with
+  // no condition on the loads themselves: slots z >= n_split re-read split
+  // n_split - 1 and get weight 0, features past DH re-read the last group and
+  // are not stored (a conditional load makes the compiler wait for each one)
   float mz[8], lz[8];
+  f32x2 ml[8];
 #pragma unroll
-  for (int z = 0; z < 8; ++z) {
-    mz[z] = z < n_split ? part_ml[((size_t)z * R + row) * 2] : -INFINITY;
-    lz[z] = z < n_split ? part_ml[((size_t)z * R + row) * 2 + 1] : 0.f;
-  }
+  for (int z = 0; z < 8; ++z)
+    ml[z] = *reinterpret_cast<const f32x2*>(part_ml + ((size_t)min(z, n_split - 1) * R + row) * 2);
   constexpr int NV = (DH + 255) / 256;  // 4-feature groups per lane
   f32x4 pv[8][NV];
 #pragma unroll
   for (int z = 0; z < 8; ++z)
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
-      const int d = 4 * lane + 256 * v;
-      pv[z][v] = (z < n_split && d < DH) ? load4_f32(part_o + ((size_t)z * R + row) * DH + d)
-                                         : f32x4{0.f, 0.f, 0.f, 0.f};
+      const int d = min(4 * lane + 256 * v, DH - 4);
+      pv[z][v] = load4_f32(part_o + ((size_t)min(z, n_split - 1) * R + row) * DH + d);
     }
+#pragma unroll
+  for (int z = 0; z < 8; ++z) {
+    mz[z] = ml[z][0];
+    lz[z] = z < n_split ? ml[z][1] : 0.f;
+  }
   float M = -INFINITY;
 #pragma unroll
   for (int z = 0; z < 8; ++z) M = fmaxf(M, mz[z]);

@@ -888,14 +888,17 @@ __global__ __launch_bounds__(256) void gemv_bias_silu_kernel(const T* __restrict
   for (int m = 0; m < kGemvRows; ++m) acc[m] = 0.f;
   const T* wrow = Bt + (size_t)n * K;
   // rows m >= M re-read row M - 1 (in bounds, never stored), so every load
-  // is unconditional and all of a k-piece's loads go out before its FMAs
-#pragma unroll 2
+  // is unconditional, and the scheduling barrier keeps all of a k-piece's
+  // loads ahead of its FMAs (left alone, the scheduler sinks each load next
+  // to its use and the wave waits for them one by one)
+#pragma unroll 1
   for (int k0 = EPV * lane; k0 < K; k0 += 64 * EPV) {
     const u32x4 wraw = *reinterpret_cast<const u32x4*>(wrow + k0);
     u32x4 araw[kGemvRows];
 #pragma unroll
     for (int m = 0; m < kGemvRows; ++m)
       araw[m] = *reinterpret_cast<const u32x4*>(A + (size_t)min(m, M - 1) * K + k0);
+    __builtin_amdgcn_sched_barrier(0);
     const T* we = reinterpret_cast<const T*>(&wraw);
 #pragma unroll
     for (int m = 0; m < kGemvRows; ++m) {

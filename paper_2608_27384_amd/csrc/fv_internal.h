@@ -25,6 +25,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // 16-byte moves (native vector)
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));  // 8-byte moves
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 // ---------------------------------------------------------------- conversions
 __device__ __forceinline__ float to_f32(float x) { return x; }
