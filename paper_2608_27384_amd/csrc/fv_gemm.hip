@@ -121,9 +121,23 @@ __device__ __forceinline__ void store_quad(T* p, const f32x4& u, bool vec) {
 // of tiles, walked in groups kTileGroup row panels tall, column by column:
 // the tiles a die runs together then share A row panels and weight column
 // blocks in its L2 instead of fetching them from memory once per die.
+// Split-K grids (gridDim.z k slices dividing the 8 dies) give each die one
+// k slice and a contiguous range of its column blocks, every row tile of
+// them: a die then fetches its slice of A and its share of the weights, not
+// the whole A of every slice.
 constexpr int kTileGroup = 8;
-__device__ __forceinline__ void tile_of(int& tm, int& tn) {
-  const int nN = gridDim.x, nM = gridDim.y, nb = nN * nM;
+__device__ __forceinline__ void tile_of(int& tm, int& tn, int& kz) {
+  const int nN = gridDim.x, nM = gridDim.y, nK = gridDim.z, nb = nN * nM;
+  kz = blockIdx.z;
+  if (nK > 1 && 8 % nK == 0 && nN % (8 / nK) == 0) {
+    const int dpk = 8 / nK;  // dies per k slice
+    const int lin = (blockIdx.z * nM + blockIdx.y) * nN + blockIdx.x;
+    const int x = lin & 7, s = lin >> 3;
+    kz = x / dpk;
+    tm = s % nM;
+    tn = (x % dpk) * (nN / dpk) + s / nM;
+    return;
+  }
   if (nb < 64) {
     tm = blockIdx.y;
     tn = blockIdx.x;
@@ -166,12 +180,11 @@ __global__ __launch_bounds__(64 * NW * KG) void gemm_kernel(const T* __restrict_
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int kg = wave / NW, wv = wave - kg * NW;  // k-group; wave within the group
   const int wm = wv % WGM, wn = wv / WGM;
-  int tm, tn;
-  tile_of(tm, tn);
+  int tm, tn, kz;
+  tile_of(tm, tn, kz);
   const int m0 = tm * BM, n0 = tn * BN;
   const int arow = wm * WTM, brow = BM + wn * WTN;  // fragment rows in the stage
   const int nk_all = K / BK;
-  const int kz = blockIdx.z;
   const int kt0 = (kz * nk_all) / KS, kt1 = ((kz + 1) * nk_all) / KS;
   const int klast = (kt1 - 1) * BK;
 
@@ -397,10 +410,10 @@ __global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(const bf16_t* __restr
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave % WGM, wn = wave / WGM;
   int tm, tn;
-  tile_of(tm, tn);
+  int kz;
+  tile_of(tm, tn, kz);
   const int m0 = tm * BM, n0 = tn * BN;
   const int nk_all = K / BK;
-  const int kz = blockIdx.z;
   const int kt0 = (kz * nk_all) / KS, kt1 = ((kz + 1) * nk_all) / KS;
 
   // lane's piece of each of the wave's loads: 16-byte unit p of a stage
