@@ -928,6 +928,88 @@ __global__ __launch_bounds__(256) void gemv_bias_silu_kernel(const T* __restrict
   }
 }
 
+// ------------------------------------------ few-row GEMM, weights streamed
+// out[m][n] = sum_k A[m][k] W[n][k] + bias[n] in fp32, bf16 operands, for
+// M <= 16 rows and a weight matrix far larger than the memory-side cache
+// (the FiLM maps of every norm at small batch), so the kernel is a stream of
+// the weights at HBM rate.  A wave owns 16 output columns at a time, whose
+// weight rows are one contiguous range, and multiplies them with MFMA
+// 16x16x32 tiles.  Lane (q, c) = (lane / 16, lane % 16) takes column c and,
+// of every 128-element k batch, the 64 contiguous bytes at k = 32q: four
+// 16-byte pieces, piece s holding k = 32q + 8s .. +8.  The MFMA's k order is
+// permuted that way on both operands, so every lane's weight loads are
+// contiguous; A, permuted once, stays in registers.  The weight pieces of
+// the next three batches (across the end of a column group, the next
+// group's first three) are in flight while one batch is multiplied.
+constexpr int kStreamRows = 16;
+template <int NB>
+__global__ __launch_bounds__(256) void stream_bias_f32_kernel(const bf16_t* __restrict__ A,
+                                                              const bf16_t* __restrict__ Bt,
+                                                              const float* __restrict__ bias,
+                                                              float* __restrict__ out, int M,
+                                                              int N) {
+  constexpr int K = 128 * NB, R = 4, AHEAD = 3;  // ring slots; batches in flight
+  static_assert(NB % R == 0 && AHEAD < R, "ring");
+  const int lane = threadIdx.x & 63, q = lane >> 4, c = lane & 15;
+  const int G = N / 16, stride = gridDim.x * 4;
+  int g = blockIdx.x + gridDim.x * (threadIdx.x >> 6);
+  if (g >= G) return;  // whole waves
+  // rows m >= M repeat row M - 1: every load is in bounds and unconditional,
+  // and those rows are never stored
+  bf16x8 a[NB][4];
+  const bf16_t* arow = A + (size_t)min(c, M - 1) * K + 32 * q;
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+      a[b][p] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(arow + 128 * b + 8 * p));
+  auto wrow = [&](int gg) { return Bt + (size_t)(16 * gg + c) * K + 32 * q; };
+  const bf16_t* cur = wrow(g);
+  u16x8 w[R][4];
+#pragma unroll
+  for (int b = 0; b < AHEAD; ++b)
+#pragma unroll
+    for (int p = 0; p < 4; ++p) w[b][p] = *reinterpret_cast<const u16x8*>(cur + 128 * b + 8 * p);
+  for (;;) {
+    // the last group's look-ahead re-reads its own first batches (cache
+    // hits) instead of another group's weights
+    const bf16_t* nxt = g + stride < G ? wrow(g + stride) : cur;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int ib = b + AHEAD;
+      const bf16_t* src = ib < NB ? cur + 128 * ib : nxt + 128 * (ib - NB);
+#pragma unroll
+      for (int p = 0; p < 4; ++p) w[ib % R][p] = *reinterpret_cast<const u16x8*>(src + 8 * p);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[b][p], __builtin_bit_cast(bf16x8, w[b % R][p]),
+                                                      acc, 0, 0, 0);
+    }
+    const int n = 16 * g + c;
+    const float bn = bias[n];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = 4 * q + r;
+      if (m < M) out[(size_t)m * N + n] = acc[r] + bn;
+    }
+    g += stride;
+    if (g >= G) break;
+    cur = nxt;
+  }
+}
+
+template <int NB>
+void launch_stream_bias_f32(const bf16_t* A, const bf16_t* Bt, const float* bias, float* out,
+                            int M, int N, hipStream_t s) {
+  // two workgroups of four waves per CU; every wave takes about G / 2048
+  // column groups
+  const int G = N / 16, blocks = std::min(512, (G + 3) / 4);
+  hipLaunchKernelGGL((stream_bias_f32_kernel<NB>), dim3(blocks), dim3(256), 0, s, A, Bt, bias, out,
+                     M, N);
+}
+
 // -------------------------------------------------------------- tile choice
 // Tile shapes (BM x BN, waves); every wave owns a sub-tile at least 64
 // columns wide, so paired epilogues find both partners of a 64-column pair
@@ -1091,6 +1173,15 @@ void gemm_bias_silu(const T* A, const T* Bt, const float* bias, T* out, int M, i
 template <typename T>
 void gemm_bias_f32(const T* A, const T* Bt, const float* bias, float* out, int M, int N, int K,
                    const GemmWork& w, hipStream_t s) {
+  if constexpr (sizeof(T) == 2) {
+    if (M <= kStreamRows && N % 16 == 0) {
+      switch (K) {
+        case 512: launch_stream_bias_f32<4>(A, Bt, bias, out, M, N, s); return;
+        case 1024: launch_stream_bias_f32<8>(A, Bt, bias, out, M, N, s); return;
+        default: break;
+      }
+    }
+  }
   run_gemm(A, Bt, M, N, K, w, EpiBiasF32{out, bias, N}, s);
 }
 template <typename T>
