@@ -119,24 +119,30 @@ def stage_kernels(w, split_k: int, n_split: int):
     mlp = (("gemv_bias_silu_kernel (time-MLP)", "gemv_bias_silu_kernel") if rows_k <= 16 else
            ("gemm<..., EpiBiasSilu> (time-MLP)", "EpiBiasSilu"))
     many = rows_t >= 4096 and w.width <= 1024
+    small_head = not many and w.width <= 1024 and w.action_dim <= 32 and w.action_dim % 4 == 0
+    stream_film = bf16 and rows_k <= 16 and w.width in (512, 1024)
     out = {
         "time_embed": ("time_embed_kernel (fp64 sinusoidal embedding)", "time_embed_kernel"),
         "time_mlp1": mlp, "time_mlp2": mlp,
-        "film_maps": ("gemm<..., EpiBiasF32> (all FiLM maps)", "EpiBiasF32"),
-        "embed": (("embed_adarms_rows_kernel" if many else "embed_adarms_kernel") +
-                  " (in-projection + first FiLM norm)",
-                  "embed_adarms_rows_kernel" if many else "embed_adarms_kernel"),
+        "film_maps": (("stream_bias_f32_kernel (all FiLM maps, weights streamed)",
+                       "stream_bias_f32_kernel") if stream_film else
+                      ("gemm<..., EpiBiasF32> (all FiLM maps)", "EpiBiasF32")),
+        "embed": ((embed := ("embed_adarms_rows_kernel" if many else
+                             "embed_adarms_small_kernel" if small_head else
+                             "embed_adarms_kernel")) + " (in-projection + first FiLM norm)", embed),
         "qkv_gemm": ("gemm_dma_kernel<..., EpiQkv> (QKV + rotary + arena)", "EpiQkv"),
         "attention": (f"{attn} (chunk-causal + prefix attention)", attn),
         "o_proj_gemm": proj, "down_proj_gemm": proj,
         "o_proj_norm": norm, "down_proj_norm": norm,
         "gate_up_gemm": ("gemm_dma_kernel<..., EpiGeglu> (gate/up + GeGLU)",
                          "EpiGeglu" if w.mlp_gated else "EpiGelu"),
-        "head": (("final_rows_kernel" if many else "final_kernel") +
-                 " (final FiLM norm + velocity head)",
-                 "final_rows_kernel" if many else "final_kernel"),
-        "euler_shift": ("euler_shift_kernel (Euler + emit + shift + refill)",
-                        "euler_shift_kernel"),
+        "head": ((head := ("final_rows_kernel" if many else
+                           "final_small_kernel" if small_head else "final_kernel")) +
+                 " (final FiLM norm + velocity head)", head),
+        "euler_shift": (("final_small_kernel<true> (Euler + emit + shift + refill fused into "
+                         "the velocity head)", "final_small_kernel<true>") if small_head else
+                        ("euler_shift_kernel (Euler + emit + shift + refill)",
+                         "euler_shift_kernel")),
     }
     if n_split > 1:
         out["attn_combine"] = ("attn_combine (merge of the key splits)", "attn_combine")

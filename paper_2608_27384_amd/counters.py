@@ -166,11 +166,17 @@ def bytes_summary(fetch_csv, write_csv, kernel, workload, launches, cmds) -> str
     return "\n".join(lines) + "\n"
 
 
+def _step_end(name: str) -> bool:
+    """A decode step ends with its Euler update: the Euler kernel, or the
+    velocity head with the update fused in."""
+    return "euler_shift_kernel" in name or "final_small_kernel<true>" in name
+
+
 def _step_window(ds) -> Tuple[int, int, int]:
     """(first, last, steps): the dispatches after the first decode step
     (warm-up) up to the end of the last one; a step ends with its Euler
-    kernel."""
-    ends = [i for i, (n, _) in enumerate(ds) if "euler_shift_kernel" in n]
+    update."""
+    ends = [i for i, (n, _) in enumerate(ds) if _step_end(n)]
     if len(ends) < 2:
         raise ValueError("need a warm-up step and at least one measured step")
     return ends[0] + 1, ends[-1], len(ends) - 1
@@ -281,15 +287,15 @@ def _kernel_table(rows: List[Tuple[str, float]]) -> List[str]:
 
 def trace_summary(trace_csv: str, workload: str, cmds: List[str]) -> str:
     """Kernel durations of a bench.py run, in two windows: the decode steps
-    (from the first time-embedding kernel to the last Euler kernel) and the
+    (from the first time-embedding kernel to the last Euler update) and the
     stage timing that follows them (one kernel replayed in a graph, layers
     cycling)."""
     rows = _rows(trace_csv)
     ev = sorted(((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"])
                  for r in rows), key=lambda x: x[0])
     first = next(i for i, e in enumerate(ev) if "time_embed_kernel" in e[2])
-    last = max(i for i, e in enumerate(ev) if "euler_shift_kernel" in e[2])
-    steps = sum(1 for e in ev[first:last + 1] if "euler_shift_kernel" in e[2])
+    last = max(i for i, e in enumerate(ev) if _step_end(e[2]))
+    steps = sum(1 for e in ev[first:last + 1] if _step_end(e[2]))
     span_us = (ev[last][1] - ev[first][0]) / 1e3
     in_step = [(n, (b - a) / 1e3) for a, b, n in ev[first:last + 1]]
     after = [(n, (b - a) / 1e3) for a, b, n in ev[last + 1:]]

@@ -216,10 +216,12 @@ int gemm_partials(const T* A, const T* Bt, int M, int N, int K, const GemmWork& 
 // ------------------------------------------------------------ other kernels
 template <typename T>
 void launch_time_embed(const float* t, T* e, int rows, int width, hipStream_t s);
+// xs (optional, only where head_fusable): a copy of x for the fused Euler
+// update of launch_final_euler.
 template <typename T>
 void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, float* h,
                          const float* mod, int mod_ld, int chunk_len, float eps, T* u, int rows,
-                         int A, int W, hipStream_t s);
+                         int A, int W, hipStream_t s, float* xs = nullptr);
 // h += gate * sum_z part[z] (split order); then, if norm_off >= 0,
 // u = rmsnorm(h) (1 + scale) + shift with the modulation at norm_off.
 // part holds bf16 values when bf16_parts, else fp32.  [pf, pf + pf_bytes)
@@ -235,6 +237,27 @@ void launch_adarms(const float* h, const float* mod, int mod_ld, int scale_off, 
 void launch_final(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
                   float eps, const float* w_out, const float* b_out, float* v, int rows, int W,
                   int A, hipStream_t s);
+// Destination of the Euler update fused into the velocity head (Algorithm 1:
+// x_k <- x_k - dt_k v_k, emit slot 0, shift, refill slot K-1): the caller's
+// buffer, the copy xs of it taken by the embedding at the start of the step,
+// t per slot, the emitted chunk, and the device noise / valid-slot state.
+struct EulerDest {
+  float* buf;
+  const float* xs;
+  const float* t;
+  float* out;
+  uint64_t* noise_state;
+  uint32_t* ticket;
+  int* n_valid;
+  int K;
+};
+// Whether the few-row head (and the fused Euler update) applies.
+bool head_fusable(int rows, int W, int A);
+// The velocity head with the Euler update, emission, shift and refill of
+// launch_euler_shift fused in (same rounding, same noise); v is not stored.
+void launch_final_euler(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
+                        float eps, const float* w_out, const float* b_out, int rows, int W, int A,
+                        const EulerDest& eu, hipStream_t s);
 void launch_euler_shift(float* buffer, const float* t, const float* v, float* out,
                         const uint64_t* noise_state, uint32_t* ticket, int* n_valid, int B, int K,
                         int CA, hipStream_t s);

@@ -142,6 +142,70 @@ __global__ __launch_bounds__(256) void embed_adarms_kernel(
   }
 }
 
+// Few rows, W <= 1024, A <= 32: kEmbSmallRows rows per block, so the grid
+// spreads over the chip; every load of the kernel (the rows of x, all of
+// w_in's rows at the thread's 4 columns, the modulation and the bias) is
+// issued before any is used, unconditionally (indices clamped, the extra
+// terms multiplied by zero), so the block waits for memory once.
+constexpr int kEmbSmallRows = 2;
+template <typename T>
+__global__ __launch_bounds__(256) void embed_adarms_small_kernel(
+    const float* __restrict__ x, const float* __restrict__ w_in, const float* __restrict__ b_in,
+    float* __restrict__ h, const float* __restrict__ mod, int mod_ld, int chunk_len, float eps,
+    T* __restrict__ u, int rows, int A, int W, float* __restrict__ xs) {
+  constexpr int R = kEmbSmallRows, AM = 32;
+  __shared__ float sred[R][4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row0 = blockIdx.x * R;
+  const int c = min(4 * tid, W - 4);
+  const bool own = 4 * tid < W;
+  float xv[R][AM];
+  f32x4 wv[AM], sv[R], bv[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int row = min(row0 + r, rows - 1);
+#pragma unroll
+    for (int a = 0; a < AM; ++a) xv[r][a] = x[(size_t)row * A + min(a, A - 1)];
+    const float* sc = mod + (size_t)(row / chunk_len) * mod_ld;
+    sv[r] = *reinterpret_cast<const f32x4*>(sc + c);
+    bv[r] = *reinterpret_cast<const f32x4*>(sc + W + c);
+  }
+#pragma unroll
+  for (int a = 0; a < AM; ++a) wv[a] = *reinterpret_cast<const f32x4*>(w_in + (size_t)min(a, A - 1) * W + c);
+  const f32x4 bias = *reinterpret_cast<const f32x4*>(b_in + c);
+  __builtin_amdgcn_sched_barrier(0);
+  // a copy of the block's rows of x for the fused Euler update (xs != null),
+  // after every other load is on its way
+  if (xs && tid < R * A && row0 * A + tid < rows * A)
+    xs[(size_t)row0 * A + tid] = x[(size_t)row0 * A + tid];
+  f32x4 acc[R];
+  float ss[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    acc[r] = bias;
+#pragma unroll
+    for (int a = 0; a < AM; ++a) acc[r] += (a < A ? xv[r][a] : 0.f) * wv[a];
+    ss[r] = own ? acc[r][0] * acc[r][0] + acc[r][1] * acc[r][1] + acc[r][2] * acc[r][2] +
+                      acc[r][3] * acc[r][3]
+                : 0.f;
+    if (own && row0 + r < rows) *reinterpret_cast<f32x4*>(h + (size_t)(row0 + r) * W + c) = acc[r];
+    const float v = wave_sum(ss[r]);
+    if (lane == 0) sred[r][wave] = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int row = row0 + r;
+    if (row >= rows || !own) continue;
+    const float tot = sred[r][0] + sred[r][1] + sred[r][2] + sred[r][3];
+    const float rinv = 1.0f / sqrtf(tot / (float)W + eps);
+    store4<T>(u + (size_t)row * W + c, acc[r][0] * rinv * (1.0f + sv[r][0]) + bv[r][0],
+              acc[r][1] * rinv * (1.0f + sv[r][1]) + bv[r][1],
+              acc[r][2] * rinv * (1.0f + sv[r][2]) + bv[r][2],
+              acc[r][3] * rinv * (1.0f + sv[r][3]) + bv[r][3]);
+  }
+}
+
 // Many rows (W <= 1024, A <= 32): thread t keeps its four columns of w_in in
 // registers and the block runs batches of kEmbRows rows through them, so
 // w_in is read once per block instead of once per batch.
@@ -416,6 +480,199 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ h,
   }
 }
 
+// ------------------------------------------------------------ Philox4x32-10
+__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+  const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+  const uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += W0;
+      k1 += W1;
+    }
+    const uint32_t hi0 = __umulhi(M0, c[0]), lo0 = M0 * c[0];
+    const uint32_t hi1 = __umulhi(M1, c[2]), lo1 = M1 * c[2];
+    const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = lo1;
+    c[2] = n2;
+    c[3] = lo0;
+  }
+}
+
+__device__ __forceinline__ void box_muller(uint32_t r0, uint32_t r1, float* z0, float* z1) {
+  const double u0 = ((double)r0 + 0.5) * 2.3283064365386962890625e-10;  // 2^-32
+  const double u1 = ((double)r1 + 0.5) * 2.3283064365386962890625e-10;
+  const double rad = sqrt(-2.0 * log(u0));
+  double s, c;
+  sincos(kTwoPi * u1, &s, &c);
+  *z0 = (float)(rad * c);
+  *z1 = (float)(rad * s);
+}
+
+// The Euler update, emission, shift and refill of one group of 4 elements
+// (group j of its chunk), with the same rounding as euler_shift_kernel: x'
+// = x - dt v, the product and the difference rounded separately.  x comes
+// from a copy of the buffer taken at the start of the step, so writing the
+// shifted slot k - 1 in place races with no reader.
+__device__ __forceinline__ void euler_group(const EulerDest& eu, f32x4 v, f32x4 x, float dt, int b,
+                                            int k, bool full, int j, size_t base, int CA,
+                                            uint64_t seed, uint64_t step) {
+#pragma clang fp contract(off)
+  float xn[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float p = dt * v[e];
+    xn[e] = x[e] - p;
+  }
+  if (k == 0) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) eu.out[(size_t)b * CA + (base - (size_t)b * eu.K * CA) + e] = full ? xn[e] : 0.f;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) eu.buf[base - CA + e] = xn[e];
+  }
+  if (k == eu.K - 1) {
+    uint32_t c[4] = {(uint32_t)j, (uint32_t)step, (uint32_t)(step >> 32), 0u};
+    const uint64_t sb = seed + (uint64_t)b;
+    philox4x32_10(c, (uint32_t)sb, (uint32_t)(sb >> 32));
+    float z[4];
+    box_muller(c[0], c[1], &z[0], &z[1]);
+    box_muller(c[2], c[3], &z[2], &z[3]);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) eu.buf[base + e] = z[e];
+  }
+}
+
+// After every block has read the step counter and the valid-slot counts,
+// the last block to finish advances them.
+__device__ __forceinline__ void euler_finish(const EulerDest& eu, int B, uint64_t step) {
+  __shared__ int s_last;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t done =
+        __hip_atomic_fetch_add(eu.ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = done == gridDim.x - 1;
+    if (s_last) {
+      eu.noise_state[1] = step + 1;
+      __hip_atomic_store(eu.ticket, 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  __syncthreads();
+  if (s_last)
+    for (int bb = threadIdx.x; bb < B; bb += blockDim.x) eu.n_valid[bb] = min(eu.n_valid[bb] + 1, eu.K);
+}
+
+// Few rows, W <= 1024, A <= 32 (A % 4 == 0): the same head with one wait
+// for memory.  Every load is issued first, unconditionally: wave w's row
+// (h, scale, shift; 16 per lane) and thread (part, q)'s 32 rows of w_out at
+// outputs 4q..4q+3, part = tid / 8 taking rows 32 part .. +32.  After the
+// normalised rows are in LDS, each thread forms its partial sums for the
+// block's rows; the 8 parts of a wave are added across lanes (lane bits 5,
+// 4, 3) and the 4 waves in a fixed order.
+__device__ __forceinline__ float sum_lane_bits_543(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(b[0]) + __uint_as_float(b[1]);
+  return dpp_add<0x128>(x);  // row_ror:8
+}
+constexpr int kFinalSmallRows = 4;
+template <bool EU>
+__global__ __launch_bounds__(256) void final_small_kernel(const float* __restrict__ h,
+                                                          const float* __restrict__ mod, int mod_ld,
+                                                          int scale_off, int chunk_len, float eps,
+                                                          const float* __restrict__ w_out,
+                                                          const float* __restrict__ b_out,
+                                                          float* __restrict__ v, int rows, int W,
+                                                          int A, EulerDest eu) {
+  constexpr int R = kFinalSmallRows, NPL = 16, KR = 32;
+  __shared__ __attribute__((aligned(16))) float su[R][1024];
+  __shared__ f32x4 sp[4][R][8];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int row0 = blockIdx.x * R;
+  const int q = tid & 7, part = tid >> 3;
+  const int qa = min(4 * q, A - 4);
+  const int k0 = part * KR;
+  // output thread (r, q) = (tid / 8, tid % 8) of the block's rows: its bias
+  // and, with the Euler update, its slot's inputs, loaded up front
+  const int orow = min(row0 + (tid >> 3 & (R - 1)), rows - 1);
+  const f32x4 bo = *reinterpret_cast<const f32x4*>(b_out + qa);
+  int ek = 0, eb = 0, nvalid = 0;
+  float dt = 0.f;
+  f32x4 x4 = {0.f, 0.f, 0.f, 0.f};
+  uint64_t seed = 0, step = 0;
+  if constexpr (EU) {
+    const int T = eu.K * chunk_len;
+    eb = orow / T;
+    ek = (orow - eb * T) / chunk_len;
+    const float tk = eu.t[(size_t)eb * eu.K + ek];
+    const float tp = eu.t[(size_t)eb * eu.K + max(ek - 1, 0)];
+    dt = tk - (ek > 0 ? tp : 0.f);
+    x4 = *reinterpret_cast<const f32x4*>(eu.xs + (size_t)orow * A + qa);
+    nvalid = eu.n_valid[eb];
+    seed = eu.noise_state[0];
+    step = eu.noise_state[1];
+  }
+  // loads: the head weights of this thread's slice, then wave's row
+  f32x4 wv[KR];
+#pragma unroll
+  for (int j = 0; j < KR; ++j)
+    wv[j] = *reinterpret_cast<const f32x4*>(w_out + (size_t)min(k0 + j, W - 1) * A + qa);
+  const int row = min(row0 + wave, rows - 1);
+  const float* hr = h + (size_t)row * W;
+  const float* sc = mod + (size_t)(row / chunk_len) * mod_ld + scale_off;
+  float hv[NPL], sv[NPL], bv[NPL];
+#pragma unroll
+  for (int i = 0; i < NPL; ++i) {
+    const int cc = min(lane + 64 * i, W - 1);
+    hv[i] = hr[cc];
+    sv[i] = sc[cc];
+    bv[i] = sc[W + cc];
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < NPL; ++i) ss += lane + 64 * i < W ? hv[i] * hv[i] : 0.f;
+  ss = wave_sum(ss);
+  const float rinv = 1.0f / sqrtf(ss / (float)W + eps);
+#pragma unroll
+  for (int i = 0; i < NPL; ++i)
+    su[wave][lane + 64 * i] = lane + 64 * i < W ? hv[i] * rinv * (1.0f + sv[i]) + bv[i] : 0.f;
+  __syncthreads();
+  // columns past W read zeros from LDS (written above), so their weights
+  // (clamped to row W - 1) contribute nothing
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < KR; j += 4) {
+      const f32x4 x4 = *reinterpret_cast<const f32x4*>(&su[r][k0 + j]);
+      acc += x4[0] * wv[j];
+      acc += x4[1] * wv[j + 1];
+      acc += x4[2] * wv[j + 2];
+      acc += x4[3] * wv[j + 3];
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] = sum_lane_bits_543(acc[e]);
+    if (lane < 8) sp[wave][r][lane] = acc;
+  }
+  __syncthreads();
+  if (tid < R * 8) {
+    const int r = tid >> 3;
+    if (row0 + r < rows && 4 * q < A) {
+      const f32x4 vv = sp[0][r][q] + sp[1][r][q] + sp[2][r][q] + sp[3][r][q] + bo;
+      if constexpr (!EU) {
+        *reinterpret_cast<f32x4*>(v + (size_t)(row0 + r) * A + 4 * q) = vv;
+      } else {
+        euler_group(eu, vv, x4, dt, eb, ek, nvalid >= eu.K, (row0 + r) % chunk_len * (A / 4) + q,
+                    (size_t)(row0 + r) * A + 4 * q, chunk_len * A, seed, step);
+      }
+    }
+  }
+  if constexpr (EU) euler_finish(eu, rows / (eu.K * chunk_len), step);
+}
+
 // Many rows (W <= 1024, A <= 32): 512 threads; thread (part, a) keeps its
 // contiguous slice (at most 64 entries) of column a of w_out in registers
 // and the block runs batches of 8 rows (one per wave) through it: w_out is
@@ -495,36 +752,6 @@ __global__ __launch_bounds__(512) void final_rows_kernel(const float* __restrict
       }
     }
   }
-}
-
-// ------------------------------------------------------------ Philox4x32-10
-__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
-  const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
-  const uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
-#pragma unroll
-  for (int r = 0; r < 10; ++r) {
-    if (r > 0) {
-      k0 += W0;
-      k1 += W1;
-    }
-    const uint32_t hi0 = __umulhi(M0, c[0]), lo0 = M0 * c[0];
-    const uint32_t hi1 = __umulhi(M1, c[2]), lo1 = M1 * c[2];
-    const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
-    c[0] = n0;
-    c[1] = lo1;
-    c[2] = n2;
-    c[3] = lo0;
-  }
-}
-
-__device__ __forceinline__ void box_muller(uint32_t r0, uint32_t r1, float* z0, float* z1) {
-  const double u0 = ((double)r0 + 0.5) * 2.3283064365386962890625e-10;  // 2^-32
-  const double u1 = ((double)r1 + 0.5) * 2.3283064365386962890625e-10;
-  const double rad = sqrt(-2.0 * log(u0));
-  double s, c;
-  sincos(kTwoPi * u1, &s, &c);
-  *z0 = (float)(rad * c);
-  *z1 = (float)(rad * s);
 }
 
 // ------------------------------------------- Euler + emit + shift + refill
@@ -706,14 +933,24 @@ void launch_time_embed(const float* t, T* e, int rows, int width, hipStream_t s)
                      width);
 }
 
+bool head_fusable(int rows, int W, int A) {
+  return rows < kManyRows && W <= 1024 && W % 4 == 0 && A <= 32 && A % 4 == 0;
+}
+
 template <typename T>
 void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, float* h,
                          const float* mod, int mod_ld, int chunk_len, float eps, T* u, int rows,
-                         int A, int W, hipStream_t s) {
+                         int A, int W, hipStream_t s, float* xs) {
   if (rows >= kManyRows && W <= 1024 && A <= 32) {
     const int rpb = kEmbRows * std::max(1, rows / (kEmbRows * kRowBlocks));
     hipLaunchKernelGGL((embed_adarms_rows_kernel<T>), dim3((rows + rpb - 1) / rpb), dim3(256), 0, s,
                        x, w_in, b_in, h, mod, mod_ld, chunk_len, eps, u, rows, A, W, rpb);
+    return;
+  }
+  if (W <= 1024 && W % 4 == 0 && A <= 32) {
+    hipLaunchKernelGGL((embed_adarms_small_kernel<T>), dim3((rows + kEmbSmallRows - 1) / kEmbSmallRows),
+                       dim3(256), 0, s, x, w_in, b_in, h, mod, mod_ld, chunk_len, eps, u, rows, A, W,
+                       xs);
     return;
   }
   const dim3 grid((rows + kEmbRows - 1) / kEmbRows);
@@ -767,8 +1004,22 @@ void launch_final(const float* h, const float* mod, int mod_ld, int scale_off, i
                        mod_ld, scale_off, chunk_len, eps, w_out, b_out, v, rows, W, A, rpb);
     return;
   }
+  if (W <= 1024 && A <= 32 && A % 4 == 0) {
+    hipLaunchKernelGGL(final_small_kernel<false>, dim3((rows + kFinalSmallRows - 1) / kFinalSmallRows),
+                       dim3(256), 0, s, h, mod, mod_ld, scale_off, chunk_len, eps, w_out, b_out, v,
+                       rows, W, A, EulerDest{});
+    return;
+  }
   hipLaunchKernelGGL(final_kernel, dim3((rows + kFinalRows - 1) / kFinalRows), dim3(256), lds, s, h, mod, mod_ld,
                      scale_off, chunk_len, eps, w_out, b_out, v, rows, W, A);
+}
+
+void launch_final_euler(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
+                        float eps, const float* w_out, const float* b_out, int rows, int W, int A,
+                        const EulerDest& eu, hipStream_t s) {
+  hipLaunchKernelGGL(final_small_kernel<true>, dim3((rows + kFinalSmallRows - 1) / kFinalSmallRows),
+                     dim3(256), 0, s, h, mod, mod_ld, scale_off, chunk_len, eps, w_out, b_out,
+                     nullptr, rows, W, A, eu);
 }
 
 void launch_euler_shift(float* buffer, const float* t, const float* v, float* out,
@@ -815,10 +1066,10 @@ template void launch_time_embed<bf16_t>(const float*, bf16_t*, int, int, hipStre
 template void launch_time_embed<float>(const float*, float*, int, int, hipStream_t);
 template void launch_embed_adarms<bf16_t>(const float*, const float*, const float*, float*,
                                           const float*, int, int, float, bf16_t*, int, int, int,
-                                          hipStream_t);
+                                          hipStream_t, float*);
 template void launch_embed_adarms<float>(const float*, const float*, const float*, float*,
                                          const float*, int, int, float, float*, int, int, int,
-                                         hipStream_t);
+                                         hipStream_t, float*);
 template void launch_resid_norm<bf16_t>(const void*, bool, int, float*, const float*, int, int,
                                         int, int, float, bf16_t*, int, int, const void*, size_t,
                                         hipStream_t);

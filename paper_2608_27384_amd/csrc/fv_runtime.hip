@@ -217,20 +217,25 @@ AttnArgs attn_args(const Handle* h, const void* kar, const void* var, int B, int
 }
 
 // Velocity pass.  `mod_cached` (FiLM maps of a static schedule) replaces the
-// time conditioning of t when given.
+// time conditioning of t when given.  With `eu` (a decode step) and a head
+// that takes it, the Euler update, emission, shift and refill run inside the
+// velocity head (the embedding keeps a copy of the buffer in h->v, which the
+// fused head reads instead of v); returns whether it did.
 template <typename T>
-void enqueue_forward(Handle* h, const float* buffer, const float* t, int B, float* v_out,
-                     int n_layers_run, hipStream_t s, const float* mod_cached) {
+bool enqueue_forward(Handle* h, const float* buffer, const float* t, int B, float* v_out,
+                     int n_layers_run, hipStream_t s, const float* mod_cached,
+                     const EulerDest* eu) {
   const int W = h->W, rowsT = B * h->T;
   const int Nmod = h->Nmod;
   const size_t layer_elems = (size_t)h->Bmax * h->Hkv * h->S * h->dh;
+  const bool fuse = eu && n_layers_run == h->L && head_fusable(rowsT, W, h->A);
   const float* mod = mod_cached;
   if (!mod) {
     enqueue_film_maps<T>(h, t, B, h->mod, s);
     mod = h->mod;
   }
   launch_embed_adarms<T>(buffer, h->w_in, h->b_in, h->hres, mod, Nmod, h->C, h->cfg.rms_eps,
-                         (T*)h->u, rowsT, h->A, W, s);
+                         (T*)h->u, rowsT, h->A, W, s, fuse ? h->v : nullptr);
   const int n_split = attn_split(h, B);
   for (int l = 0; l < n_layers_run; ++l) {
     T* kar = (T*)h->karena + l * layer_elems;
@@ -256,9 +261,17 @@ void enqueue_forward(Handle* h, const float* buffer, const float* t, int B, floa
                    next_norm, rowsT, s, l + 1 < h->L ? h->wqkv[l + 1] : nullptr,
                    (size_t)h->Nqkv * W * h->esz);
   }
+  if (fuse) {
+    EulerDest d = *eu;
+    d.xs = h->v;
+    launch_final_euler(h->hres, mod, Nmod, 6 * h->L * W, h->C, h->cfg.rms_eps, h->w_out,
+                       h->b_out, rowsT, W, h->A, d, s);
+    return true;
+  }
   if (v_out)
     launch_final(h->hres, mod, Nmod, 6 * h->L * W, h->C, h->cfg.rms_eps, h->w_out, h->b_out,
                  v_out, rowsT, W, h->A, s);
+  return false;
 }
 
 // One projection GEMM with the gated residual, alone: the split-K partials
@@ -354,12 +367,21 @@ void run_stage(Handle* h, int stage, int l, hipStream_t s) {
   }
 }
 
-void forward(Handle* h, const float* buffer, const float* t, int B, float* v_out, int n_layers,
-             hipStream_t s, const float* mod_cached = nullptr) {
+bool forward(Handle* h, const float* buffer, const float* t, int B, float* v_out, int n_layers,
+             hipStream_t s, const float* mod_cached = nullptr, const EulerDest* eu = nullptr) {
   if (h->bf16)
-    enqueue_forward<bf16_t>(h, buffer, t, B, v_out, n_layers, s, mod_cached);
-  else
-    enqueue_forward<float>(h, buffer, t, B, v_out, n_layers, s, mod_cached);
+    return enqueue_forward<bf16_t>(h, buffer, t, B, v_out, n_layers, s, mod_cached, eu);
+  return enqueue_forward<float>(h, buffer, t, B, v_out, n_layers, s, mod_cached, eu);
+}
+
+// One decode step (Algorithm 1): the velocity pass, then the Euler update,
+// emission, shift and refill, fused into the velocity head where it can be.
+void decode(Handle* h, float* buffer, const float* t, int B, float* out_chunk, hipStream_t s,
+            const float* mod_cached) {
+  const EulerDest eu{buffer, nullptr, t, out_chunk, h->d_noise, h->d_ticket, h->d_valid, h->K};
+  if (!forward(h, buffer, t, B, h->v, h->L, s, mod_cached, &eu))
+    launch_euler_shift(buffer, t, h->v, out_chunk, h->d_noise, h->d_ticket, h->d_valid, B, h->K,
+                       h->C * h->A, s);
 }
 
 void film_maps(Handle* h, const float* t, int B, float* mod, hipStream_t s) {
@@ -929,11 +951,7 @@ fv_status fv_decode_step(fv_handle h, float* buffer, const float* t, float* out_
     hipStream_t st = static_cast<hipStream_t>(stream);
     activate_staged(h, st);
     run_step(h, t ? KIND_STEP : KIND_STEP_CACHED, buffer, tt, out_chunk, nullptr, 0, st,
-             [&](hipStream_t s) {
-               forward(h, buffer, tt, B, h->v, h->L, s, mod);
-               launch_euler_shift(buffer, tt, h->v, out_chunk, h->d_noise, h->d_ticket,
-                                  h->d_valid, B, h->K, h->C * h->A, s);
-             });
+             [&](hipStream_t s) { decode(h, buffer, tt, B, out_chunk, s, mod); });
     mark_used(h, st);
   });
 }
@@ -965,9 +983,7 @@ fv_status fv_decode_step_noalloc(fv_handle h, float* buffer, const float* t, flo
     {
       ScratchSwap sw(h, base, need);
       (void)hipGetLastError();
-      forward(h, buffer, tt, B, h->v, h->L, st, mod);
-      launch_euler_shift(buffer, tt, h->v, out_chunk, h->d_noise, h->d_ticket, h->d_valid, B,
-                         h->K, h->C * h->A, st);
+      decode(h, buffer, tt, B, out_chunk, st, mod);
       check_launch();
     }
     mark_used(h, st);
