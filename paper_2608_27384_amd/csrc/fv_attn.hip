@@ -30,6 +30,9 @@
 // query for 4 keys per 16-key subtile; the row max and row sum need only two
 // cross-lane exchanges (lanes l, l^16, l^32, l^48); the probabilities are
 // then, without any data movement, the B operand of O^T += V^T P^T.
+#include <algorithm>
+#include <vector>
+
 #include "fv_internal.h"
 
 namespace fv {
@@ -373,7 +376,10 @@ __device__ __forceinline__ void wait_lgkmcnt0_attn() {
 // blocks of a die take a contiguous range of the (stream-major) work list,
 // so the row tiles of one stream, which read the same keys and values, run
 // together on one die instead of being spread over all eight.
-__device__ __forceinline__ void attn_block_of(int& rtile, int& bg) {
+// The list is walked in die_order, which gives every die about the same
+// total prefix length (ragged prefixes otherwise leave some dies a seventh
+// more work than others).
+__device__ __forceinline__ void attn_block_of(int& rtile, int& bg, const int* __restrict__ order) {
   const int nx = gridDim.x, nb = nx * gridDim.y;
   if (gridDim.z > 1 || nb < 64) {
     rtile = blockIdx.x;
@@ -384,8 +390,9 @@ __device__ __forceinline__ void attn_block_of(int& rtile, int& bg) {
   const int per = nb >> 3, rem = nb & 7;
   const int x = blk & 7, slot = blk >> 3;
   const int L = x * per + min(x, rem) + slot;
-  bg = L / nx;
-  rtile = L - bg * nx;
+  const int pos = L / nx;
+  bg = order[pos];
+  rtile = L - pos * nx;
 }
 
 template <int DH, int NWV>
@@ -406,7 +413,7 @@ __global__ __launch_bounds__(64 * NWV) void attn16_kernel(AttnArgs a) {
   const int G = a.n_q_heads / a.n_kv_heads;
   const int rows_bg = a.tokens * G;
   int rtile, bg;
-  attn_block_of(rtile, bg);
+  attn_block_of(rtile, bg, a.bg_order);
   const int tile0 = rtile * RB;
   const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
   const int split = blockIdx.z;
@@ -662,7 +669,7 @@ __global__ __launch_bounds__(64 * NWV) void attn16d_kernel(AttnArgs a) {
   const int G = a.n_q_heads / a.n_kv_heads;
   const int rows_bg = a.tokens * G;
   int rtile, bg;
-  attn_block_of(rtile, bg);
+  attn_block_of(rtile, bg, a.bg_order);
   const int tile0 = rtile * RB;
   const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
   const int split = blockIdx.z;
@@ -983,6 +990,29 @@ void launch_dh(const AttnArgs& a, hipStream_t s, int parts) {
 }
 
 }  // namespace
+
+void die_order(const int* len, int B, int Hkv, int* order) {
+  const int n = B * Hkv;
+  for (int i = 0; i < n; ++i) order[i] = i;
+  if (n % 8 || n < 8) return;
+  // longest first, each to the least-loaded die with room left
+  std::vector<int> byl(order, order + n);
+  std::stable_sort(byl.begin(), byl.end(),
+                   [&](int x, int y) { return len[x / Hkv] > len[y / Hkv]; });
+  const int cap = n / 8;
+  std::vector<std::vector<int>> die(8);
+  std::vector<long> load(8, 0);
+  for (int bg : byl) {
+    int best = -1;
+    for (int d = 0; d < 8; ++d)
+      if ((int)die[d].size() < cap && (best < 0 || load[d] < load[best])) best = d;
+    die[best].push_back(bg);
+    load[best] += len[bg / Hkv];
+  }
+  int k = 0;
+  for (int d = 0; d < 8; ++d)
+    for (int bg : die[d]) order[k++] = bg;
+}
 
 template <typename T>
 int attention_row_tiles(int tokens, int n_q_heads, int n_kv_heads) {

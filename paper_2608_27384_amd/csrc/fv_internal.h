@@ -290,7 +290,15 @@ struct AttnArgs {
   int mask_mode;        // FV_MASK_*
   const void* pf;       // prefetched into the memory-side cache meanwhile (or nullptr)
   size_t pf_bytes;
+  const int* bg_order;  // [B*Hkv] (stream, kv head) pairs in die order (die_order)
 };
+
+// The (stream, kv head) pairs in the order in which a large attention grid
+// hands them to the 8 dies (die x takes the x-th eighth of the list): each
+// die gets the same number of pairs and about the same total prefix length,
+// the longest pairs first within a die.  Identity when B*Hkv is not a
+// multiple of 8.
+void die_order(const int* len, int B, int Hkv, int* order);
 
 // Buffer chunks [lo, hi) visible to the queries of chunk kq (see the mask
 // modes in the C header); slots before `first` are cold-start padding.
@@ -345,7 +353,8 @@ struct Handle {
   void* karena = nullptr;   // [L][Bmax][Hkv][S][dh]
   void* vtarena = nullptr;  // [L][Bmax][Hkv][dh][S]
   int* d_len = nullptr;
-  std::vector<int32_t> len_host;
+  std::vector<int32_t> len_host;   // followed on the device (d_len + Bmax) by die_order
+  std::vector<int32_t> order_host;
   int batch = 0;
   bool prefix_set = false;
 

@@ -213,7 +213,7 @@ AttnArgs attn_args(const Handle* h, const void* kar, const void* var, int B, int
   return AttnArgs{h->q,  kar,      var,  h->d_len, h->o,          h->part_o,
                   h->part_ml, B,   h->T, h->C,     h->Hq,         h->Hkv,
                   h->dh, h->S,     n_split, h->d_valid, h->mask_mode, FV_PREFETCH ? pf : nullptr,
-                  pf_bytes};
+                  pf_bytes, h->d_len + h->Bmax};
 }
 
 // Velocity pass.  `mod_cached` (FiLM maps of a static schedule) replaces the
@@ -770,8 +770,9 @@ fv_status fv_create(const fv_weights* w, const fv_cfg* cfg, fv_handle* out) {
     H.vtarena = dalloc(h, arena);
     FV_HIP(hipMemset(H.karena, 0, arena));
     FV_HIP(hipMemset(H.vtarena, 0, arena));
-    H.d_len = static_cast<int*>(dalloc(h, (size_t)H.Bmax * 4));
-    FV_HIP(hipMemset(H.d_len, 0, (size_t)H.Bmax * 4));
+    // [len | die_order]: Bmax lengths, then the Bmax*Hkv (stream, kv head) order
+    H.d_len = static_cast<int*>(dalloc(h, (size_t)H.Bmax * (1 + H.Hkv) * 4));
+    FV_HIP(hipMemset(H.d_len, 0, (size_t)H.Bmax * (1 + H.Hkv) * 4));
     H.arena_k[0] = H.karena;
     H.arena_v[0] = H.vtarena;
     H.len_slot[0] = H.d_len;
@@ -849,7 +850,11 @@ fv_status fv_set_prefix(fv_handle h, const void* k, const void* v, const int32_t
     hipStream_t s = static_cast<hipStream_t>(stream);
     h->staged_slot = -1;  // a pending asynchronous observation is superseded
     h->len_host.assign(len_host, len_host + batch);
+    h->order_host.resize((size_t)batch * h->Hkv);
+    die_order(h->len_host.data(), batch, h->Hkv, h->order_host.data());
     FV_HIP(hipMemcpyAsync(h->d_len, h->len_host.data(), (size_t)batch * 4, hipMemcpyHostToDevice, s));
+    FV_HIP(hipMemcpyAsync(h->d_len + h->Bmax, h->order_host.data(), h->order_host.size() * 4,
+                          hipMemcpyHostToDevice, s));
     if (ld > 0 && maxlen > 0) {
       if (h->bf16)
         launch_prefix_copy<bf16_t>((const bf16_t*)k, (const bf16_t*)v, h->L, batch, batch, ld,
@@ -889,15 +894,15 @@ fv_status fv_set_prefix_async(fv_handle h, const void* k, const void* v, const i
       const size_t arena = (size_t)h->L * h->Bmax * h->Hkv * h->S * h->dh * h->esz;
       h->arena_k[1] = dalloc(h, arena);
       h->arena_v[1] = dalloc(h, arena);
-      h->len_slot[1] = static_cast<int*>(dalloc(h, (size_t)h->Bmax * 4));
+      h->len_slot[1] = static_cast<int*>(dalloc(h, (size_t)h->Bmax * (1 + h->Hkv) * 4));
       FV_HIP(hipMemset(h->arena_k[1], 0, arena));
       FV_HIP(hipMemset(h->arena_v[1], 0, arena));
       for (int i = 0; i < 2; ++i) {
         FV_HIP(hipEventCreateWithFlags(&h->ev_ready[i], hipEventDisableTiming));
         FV_HIP(hipEventCreateWithFlags(&h->ev_done[i], hipEventDisableTiming));
         FV_HIP(hipEventCreateWithFlags(&h->ev_len[i], hipEventDisableTiming));
-        FV_HIP(hipHostMalloc(reinterpret_cast<void**>(&h->pinned_len[i]), (size_t)h->Bmax * 4,
-                             hipHostMallocDefault));
+        FV_HIP(hipHostMalloc(reinterpret_cast<void**>(&h->pinned_len[i]),
+                             (size_t)h->Bmax * (1 + h->Hkv) * 4, hipHostMallocDefault));
       }
       h->async_ready = true;
     }
@@ -909,9 +914,12 @@ fv_status fv_set_prefix_async(fv_handle h, const void* k, const void* v, const i
     if (h->staged_slot >= 0) FV_HIP(hipStreamWaitEvent(cs, h->ev_ready[sl], 0));
     if (h->len_recorded[sl]) FV_HIP(hipEventSynchronize(h->ev_len[sl]));
     std::memcpy(h->pinned_len[sl], len_host, (size_t)batch * 4);
+    die_order(h->pinned_len[sl], batch, h->Hkv, h->pinned_len[sl] + h->Bmax);
     (void)hipGetLastError();
     FV_HIP(hipMemcpyAsync(h->len_slot[sl], h->pinned_len[sl], (size_t)batch * 4,
                           hipMemcpyHostToDevice, cs));
+    FV_HIP(hipMemcpyAsync(h->len_slot[sl] + h->Bmax, h->pinned_len[sl] + h->Bmax,
+                          (size_t)batch * h->Hkv * 4, hipMemcpyHostToDevice, cs));
     FV_HIP(hipEventRecord(h->ev_len[sl], cs));
     h->len_recorded[sl] = true;
     if (ld > 0 && maxlen > 0) {
@@ -1102,9 +1110,13 @@ fv_status fv_multibuffer_velocity(fv_handle h, const void* k, const void* v, int
     // holds j real chunks after N - j padding slots
     h->staged_slot = -1;  // a pending asynchronous observation is superseded
     h->len_host.assign(N, prefix_len);
+    h->order_host.resize((size_t)N * h->Hkv);
+    die_order(h->len_host.data(), N, h->Hkv, h->order_host.data());
     std::vector<int> valid(N);
     for (int j = 0; j < N; ++j) valid[j] = j + 1;
     FV_HIP(hipMemcpyAsync(h->d_len, h->len_host.data(), (size_t)N * 4, hipMemcpyHostToDevice, s));
+    FV_HIP(hipMemcpyAsync(h->d_len + h->Bmax, h->order_host.data(), h->order_host.size() * 4,
+                          hipMemcpyHostToDevice, s));
     FV_HIP(hipMemcpyAsync(h->d_valid, valid.data(), (size_t)N * 4, hipMemcpyHostToDevice, s));
     if (ld > 0 && prefix_len > 0) {
       if (h->bf16)
