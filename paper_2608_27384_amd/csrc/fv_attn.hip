@@ -378,7 +378,7 @@ __device__ __forceinline__ void wait_lgkmcnt0_attn() {
 // together on one die instead of being spread over all eight.
 // The list is walked in die_order, which gives every die about the same
 // total prefix length (ragged prefixes otherwise leave some dies a seventh
-// more work than others).
+// more work than others), and a stream's row tiles from the last.
 __device__ __forceinline__ void attn_block_of(int& rtile, int& bg, const int* __restrict__ order) {
   const int nx = gridDim.x, nb = nx * gridDim.y;
   if (gridDim.z > 1 || nb < 64) {
@@ -392,7 +392,8 @@ __device__ __forceinline__ void attn_block_of(int& rtile, int& bg, const int* __
   const int L = x * per + min(x, rem) + slot;
   const int pos = L / nx;
   bg = order[pos];
-  rtile = L - pos * nx;
+  // a stream's last row tiles see the most buffer keys: they go first
+  rtile = nx - 1 - (L - pos * nx);
 }
 
 template <int DH, int NWV>
