@@ -517,21 +517,24 @@ def measure_async_pipeline(w, steps=60, warmup=6, hz=30.0, horizons=(16, 5, 2),
     obs = _observations(w, 2)
     res = {"workload": w.name, "batch": w.batch, "steps": steps, "executor_hz": hz,
            "horizons_E": list(horizons)}
-    loop = {}
-    for mode in modes:
-        ex = Expert(inp.W, w, w.batch, w.max_prefix, noise_seed=w.noise_seed)
-        try:
+    # The modes run interleaved, in rounds of steps / rounds control steps
+    # with the order rotating from round to round, so that a drift of the
+    # GPU's clock over the run does not favour the mode measured first.
+    loop, ctl, handles = {}, {}, []
+    try:
+        main = torch.cuda.current_stream()
+        for mode in modes:
+            ex = Expert(inp.W, w, w.batch, w.max_prefix, noise_seed=w.noise_seed)
+            handles.append(ex)
             xd = torch.from_numpy(inp.x.copy()).cuda()
             td = torch.from_numpy(inp.t).cuda()
             out = torch.empty((w.batch, w.chunk_len, w.action_dim), dtype=torch.float32,
                               device="cuda")
-            main = torch.cuda.current_stream()
             cs = torch.cuda.Stream() if mode == "pipelined_copy_stream" else main
             kd, vd, lens = obs[0]
             ex.set_prefix(kd, vd, lens)
-            state = {"i": 0}
 
-            def control_step():
+            def control_step(mode=mode, ex=ex, xd=xd, td=td, out=out, cs=cs, state={"i": 0}):
                 i = state["i"]
                 state["i"] += 1
                 kd, vd, lens = obs[(i + 1) % 2]
@@ -541,11 +544,22 @@ def measure_async_pipeline(w, steps=60, warmup=6, hz=30.0, horizons=(16, 5, 2),
                 else:
                     ex.set_prefix_async(kd, vd, lens, cs)  # next observation, no wait
 
-            per, total_ms, wall = time_steps(control_step, steps, warmup)
+            ctl[mode] = control_step
+            for _ in range(warmup):
+                control_step()
             torch.cuda.synchronize()
-            loop[mode] = {"ms_per_control_step": wall * 1e3 / steps,
-                          "gpu_ms_per_control_step": total_ms / steps}
-        finally:
+            loop[mode] = {"ms_per_control_step": 0.0, "gpu_ms_per_control_step": 0.0}
+        rounds = max(1, min(6, steps // 5))
+        per_round = steps // rounds
+        for r in range(rounds):
+            k = r % len(modes)
+            for mode in modes[k:] + modes[:k]:
+                _, total_ms, wall = time_steps(ctl[mode], per_round, 0)
+                loop[mode]["ms_per_control_step"] += wall * 1e3 / (per_round * rounds)
+                loop[mode]["gpu_ms_per_control_step"] += total_ms / (per_round * rounds)
+        torch.cuda.synchronize()
+    finally:
+        for ex in handles:
             ex.close()
     res["control_loop"] = loop
     if not timeline:
