@@ -80,8 +80,8 @@ def step_flops(w, lens):
     W, L, F, A = w.width, w.n_layers, w.mlp_dim, w.action_dim
     qd, kd = w.n_q_heads * w.head_dim, w.n_kv_heads * w.head_dim
     ngu = 2 * F if w.mlp_gated else F
-    rows_t, rows_k = w.batch * w.tokens, w.batch * w.n_chunks
-    gemm = 2 * rows_k * W * W * 2 + 2 * rows_k * W * (6 * L + 2) * W
+    rows_t, rows_f = w.batch * w.tokens, film_rows(w)
+    gemm = 2 * rows_f * W * W * 2 + 2 * rows_f * W * (6 * L + 2) * W
     gemm += 2 * rows_t * A * W * 2
     gemm += L * 2 * rows_t * (W * (qd + 2 * kd) + qd * W + W * ngu + F * W)
     attn = sum(4 * w.head_dim * w.n_q_heads * visible_pairs(w, p) * L for p in lens)
@@ -101,11 +101,18 @@ DEBUG_STAGES = {"film_maps": 0, "qkv_gemm": 1, "gate_up_gemm": 3, "attention": 4
                 "down_proj_norm": 11}
 
 
+def film_rows(w):
+    """FiLM-map rows a step computes: with several streams whose noise levels
+    are the same staircase (these inputs), stream 0's K rows serve them all."""
+    return w.n_chunks if w.batch > 1 else w.batch * w.n_chunks
+
+
 def stage_kernels(w, split_k: int, n_split: int):
     """Stage -> (kernel label, substring of the kernel's name in a rocprofv3
     trace).  Stages that launch the same kernel share a label."""
     bf16 = w.dtype == synth.BF16
     rows_k, rows_t = w.batch * w.n_chunks, w.batch * w.tokens
+    rows_f = film_rows(w)
     if bf16:
         attn = ("attn16d_kernel" if w.head_dim in (128, 256) else "attn16_kernel")
     else:
@@ -116,11 +123,11 @@ def stage_kernels(w, split_k: int, n_split: int):
              "EpiGatedResid"))
     norm = (("resid_norm_kernel (split-K sum + gated residual + FiLM norm)", "resid_norm_kernel")
             if split_k > 1 else ("adarms_kernel (FiLM norm)", "adarms_kernel"))
-    mlp = (("gemv_bias_silu_kernel (time-MLP)", "gemv_bias_silu_kernel") if rows_k <= 16 else
+    mlp = (("gemv_bias_silu_kernel (time-MLP)", "gemv_bias_silu_kernel") if rows_f <= 16 else
            ("gemm<..., EpiBiasSilu> (time-MLP)", "EpiBiasSilu"))
     many = rows_t >= 4096 and w.width <= 1024
     small_head = not many and w.width <= 1024 and w.action_dim <= 32 and w.action_dim % 4 == 0
-    stream_film = bf16 and rows_k <= 16 and w.width in (512, 1024)
+    stream_film = bf16 and rows_f <= 16 and w.width in (512, 1024)
     out = {
         "time_embed": ("time_embed_kernel (fp64 sinusoidal embedding)", "time_embed_kernel"),
         "time_mlp1": mlp, "time_mlp2": mlp,
@@ -164,6 +171,7 @@ def stage_work(w, lens, n_split: int, split_k: int):
     qd, kd = w.n_q_heads * w.head_dim, w.n_kv_heads * w.head_dim
     ngu = 2 * F if w.mlp_gated else F
     rows_t, rows_k = w.batch * w.tokens, w.batch * w.n_chunks
+    rows_f = film_rows(w)
     nmod = (6 * w.n_layers + 2) * W
     kv_bytes = 2 * (int(np.sum(lens)) + rows_t) * kd * e
     R = rows_t * w.n_q_heads
@@ -179,12 +187,12 @@ def stage_work(w, lens, n_split: int, split_k: int):
     buf = w.batch * w.tokens * A * 4
     return {
         "time_embed": (0, rows_k * 4 + rows_k * W * e),
-        "time_mlp1": (2 * rows_k * W * W, W * W * e + W * 4 + 2 * rows_k * W * e),
-        "time_mlp2": (2 * rows_k * W * W, W * W * e + W * 4 + 2 * rows_k * W * e),
+        "time_mlp1": (2 * rows_f * W * W, W * W * e + W * 4 + 2 * rows_f * W * e),
+        "time_mlp2": (2 * rows_f * W * W, W * W * e + W * 4 + 2 * rows_f * W * e),
         "embed": (2 * rows_t * A * W, buf + (A + 1) * W * 4 + rows_t * W * (4 + e)),
         "head": (2 * rows_t * W * A, rows_t * W * 4 + (W + 1) * A * 4 + buf),
         "euler_shift": (0, 3 * buf + w.batch * C * A * 4 + rows_k * 4),
-        "film_maps": (2 * rows_k * W * nmod, nmod * W * e + nmod * 4 + rows_k * (W * e + nmod * 4)),
+        "film_maps": (2 * rows_f * W * nmod, nmod * W * e + nmod * 4 + rows_f * (W * e + nmod * 4)),
         "qkv_gemm": (2 * rows_t * W * (qd + 2 * kd), W * (qd + 2 * kd) * e + rows_t * W * e
                      + rows_t * (qd + 2 * kd) * e),
         "attention": (sum(4 * w.head_dim * w.n_q_heads * visible_pairs(w, p) for p in lens),

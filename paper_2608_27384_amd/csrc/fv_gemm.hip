@@ -154,11 +154,23 @@ __device__ __forceinline__ void tile_of(int& tm, int& tn, int& kz) {
   tn = i / gm;
 }
 
+// Epilogues with a run-time skip flag (Epi::skipped()): the whole launch
+// returns at once when it is set (every workgroup reads the same flag).
+template <class Epi, class = void>
+struct EpiSkip {
+  __device__ static bool skip(const Epi&) { return false; }
+};
+template <class Epi>
+struct EpiSkip<Epi, std::void_t<decltype(&Epi::skipped)>> {
+  __device__ static bool skip(const Epi& e) { return e.skipped(); }
+};
+
 template <typename T, int BM, int BN, int NW, int WGM, int KG, class Epi>
 __global__ __launch_bounds__(64 * NW * KG) void gemm_kernel(const T* __restrict__ A,
                                                             const T* __restrict__ Bt, int M,
                                                             int N, int K, int KS,
                                                             float* __restrict__ ws, Epi epi) {
+  if (EpiSkip<Epi>::skip(epi)) return;
   using MF = Mf32<T>;
   constexpr int NT = 64 * NW * KG;
   constexpr int WGN = NW / WGM;
@@ -394,6 +406,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(const bf16_t* __restr
                                                            const bf16_t* __restrict__ Bt, int M,
                                                            int N, int K, int KS,
                                                            float* __restrict__ ws, Epi epi) {
+  if (EpiSkip<Epi>::skip(epi)) return;
   constexpr int WGN = NW / WGM, WTM = BM / WGM, WTN = BN / WGN, FM = WTM / 32, FN = WTN / 32;
   constexpr int BK = 64, NSTEP = 4;
   // k-steps whose fragments are read ahead: two for the 32x64 wave tiles,
@@ -558,6 +571,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(const bf16_t* __restr
 template <int BM, int BN, int NW, int WGM, class Epi>
 __global__ __launch_bounds__(64 * NW) void gemm_reduce_kernel(const float* __restrict__ ws, int M,
                                                               int N, int KS, Epi epi) {
+  if (EpiSkip<Epi>::skip(epi)) return;
   constexpr int WGN = NW / WGM;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int FM = WTM / 32, FN = WTN / 32;
@@ -599,6 +613,8 @@ struct EpiNone {
 template <typename T>
 struct EpiBiasSilu {
   T* out; const float* bias; int ldo;
+  const int* skip;  // nullptr, or a flag that skips the launch when set
+  __device__ bool skipped() const { return skip && *skip; }
   template <int FM, int FN>
   __device__ void apply(f32x16 (&acc)[FM][FN], int row0, int col0, int lane, int M) const {
 #pragma unroll
@@ -618,6 +634,8 @@ struct EpiBiasSilu {
 
 struct EpiBiasF32 {
   float* out; const float* bias; int ldo;
+  const int* skip;  // nullptr, or a flag that skips the launch when set
+  __device__ bool skipped() const { return skip && *skip; }
   template <int FM, int FN>
   __device__ void apply(f32x16 (&acc)[FM][FN], int row0, int col0, int lane, int M) const {
 #pragma unroll
@@ -756,6 +774,7 @@ struct EpiQkv {
 struct EpiGatedResid {
   static constexpr bool kStaged = true;
   float* h; const float* mod; int mod_ld, gate_off, chunk_len, ldh;
+  const int* period;  // FiLM-row sharing flag (film_row), or nullptr
   // Direct-to-LDS kernels: the accumulators go through the (idle) LDS so that
   // h is read and written as whole-row 16-byte pieces, in passes of PI
   // 32-row slabs per wave; `smem` holds NW x PI x 32 x WTN floats.
@@ -768,6 +787,7 @@ struct EpiGatedResid {
     static_assert(PI >= 1 && FM % PI == 0, "staging does not fit");
     constexpr int C4 = WTN / 4;                // 16-byte pieces per row
     constexpr int PER = PI * 32 * C4 / 64;     // pieces per lane and pass
+    const int per = film_period(period);
     float* cs = smem + wave * PI * 32 * WTN;
     float* __restrict__ hh = h;
     const float* __restrict__ mm = mod;
@@ -791,7 +811,7 @@ struct EpiGatedResid {
           const int idx = (q0 + q) * 64 + lane, rr = idx / C4, c4 = idx - rr * C4;
           const int row = min(row0 + 32 * i0 + rr, M - 1);
           hv[q] = *reinterpret_cast<const f32x4*>(hh + (size_t)row * ldh + col0 + 4 * c4);
-          gv[q] = *reinterpret_cast<const f32x4*>(mm + (size_t)(row / chunk_len) * mod_ld +
+          gv[q] = *reinterpret_cast<const f32x4*>(mm + (size_t)film_row(row / chunk_len, per) * mod_ld +
                                                   gate_off + col0 + 4 * c4);
         }
 #pragma unroll
@@ -808,6 +828,7 @@ struct EpiGatedResid {
   }
   template <int FM, int FN>
   __device__ void apply(f32x16 (&acc)[FM][FN], int row0, int col0, int lane, int M) const {
+    const int per = film_period(period);
     float* __restrict__ hh = h;
     const float* __restrict__ mm = mod;
 #pragma unroll
@@ -820,7 +841,7 @@ struct EpiGatedResid {
         for (int r = 0; r < 16; ++r) {  // independent loads first
           const int row = min(row0 + 32 * i + acc_row(r, lane), M - 1);
           hv[r] = hh[(size_t)row * ldh + col];
-          gv[r] = mm[(size_t)(row / chunk_len) * mod_ld + gate_off + col];
+          gv[r] = mm[(size_t)film_row(row / chunk_len, per) * mod_ld + gate_off + col];
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -892,7 +913,8 @@ __global__ __launch_bounds__(256) void gemv_bias_silu_kernel(const T* __restrict
                                                              const T* __restrict__ Bt,
                                                              const float* __restrict__ bias,
                                                              T* __restrict__ out, int M, int N,
-                                                             int K) {
+                                                             int K, const int* __restrict__ skip) {
+  if (skip && *skip) return;
   constexpr int EPV = 16 / (int)sizeof(T);  // elements per 16-byte piece
   const int lane = threadIdx.x & 63;
   const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -947,7 +969,8 @@ __global__ __launch_bounds__(256) void stream_bias_f32_kernel(const bf16_t* __re
                                                               const bf16_t* __restrict__ Bt,
                                                               const float* __restrict__ bias,
                                                               float* __restrict__ out, int M,
-                                                              int N) {
+                                                              int N, const int* __restrict__ skip) {
+  if (skip && *skip) return;
   constexpr int K = 128 * NB, R = 4, AHEAD = 3;  // ring slots; batches in flight
   static_assert(NB % R == 0 && AHEAD < R, "ring");
   const int lane = threadIdx.x & 63, q = lane >> 4, c = lane & 15;
@@ -1002,13 +1025,13 @@ __global__ __launch_bounds__(256) void stream_bias_f32_kernel(const bf16_t* __re
 
 template <int NB>
 void launch_stream_bias_f32(const bf16_t* A, const bf16_t* Bt, const float* bias, float* out,
-                            int M, int N, hipStream_t s) {
+                            int M, int N, hipStream_t s, const int* skip) {
   // one workgroup of four waves per CU, every wave about G / 1024 column
   // groups (a cold read of the FiLM weights: 48.5 us against 50.4 with two
   // workgroups per CU, and 46.6 for a plain streaming read of the same bytes)
   const int G = N / 16, blocks = std::min(256, (G + 3) / 4);
   hipLaunchKernelGGL((stream_bias_f32_kernel<NB>), dim3(blocks), dim3(256), 0, s, A, Bt, bias, out,
-                     M, N);
+                     M, N, skip);
 }
 
 // -------------------------------------------------------------- tile choice
@@ -1163,27 +1186,27 @@ int gemm_partials(const T* A, const T* Bt, int M, int N, int K, const GemmWork& 
 
 template <typename T>
 void gemm_bias_silu(const T* A, const T* Bt, const float* bias, T* out, int M, int N, int K,
-                    const GemmWork& w, hipStream_t s) {
+                    const GemmWork& w, hipStream_t s, const int* skip) {
   if (M <= kGemvRows && N % 4 == 0 && K % (16 / (int)sizeof(T)) == 0) {
     hipLaunchKernelGGL((gemv_bias_silu_kernel<T>), dim3(N / 4), dim3(256), 0, s, A, Bt, bias, out,
-                       M, N, K);
+                       M, N, K, skip);
     return;
   }
-  run_gemm(A, Bt, M, N, K, w, EpiBiasSilu<T>{out, bias, N}, s);
+  run_gemm(A, Bt, M, N, K, w, EpiBiasSilu<T>{out, bias, N, skip}, s);
 }
 template <typename T>
 void gemm_bias_f32(const T* A, const T* Bt, const float* bias, float* out, int M, int N, int K,
-                   const GemmWork& w, hipStream_t s) {
+                   const GemmWork& w, hipStream_t s, const int* skip) {
   if constexpr (sizeof(T) == 2) {
     if (M <= kStreamRows && N % 16 == 0) {
       switch (K) {
-        case 512: launch_stream_bias_f32<4>(A, Bt, bias, out, M, N, s); return;
-        case 1024: launch_stream_bias_f32<8>(A, Bt, bias, out, M, N, s); return;
+        case 512: launch_stream_bias_f32<4>(A, Bt, bias, out, M, N, s, skip); return;
+        case 1024: launch_stream_bias_f32<8>(A, Bt, bias, out, M, N, s, skip); return;
         default: break;
       }
     }
   }
-  run_gemm(A, Bt, M, N, K, w, EpiBiasF32{out, bias, N}, s);
+  run_gemm(A, Bt, M, N, K, w, EpiBiasF32{out, bias, N, skip}, s);
 }
 template <typename T>
 void gemm_qkv(const T* A, const T* Bt, const QkvArgs<T>& qa, int M, int N, int K,
@@ -1193,8 +1216,8 @@ void gemm_qkv(const T* A, const T* Bt, const QkvArgs<T>& qa, int M, int N, int K
 template <typename T>
 void gemm_gated_resid(const T* A, const T* Bt, float* h, const float* mod, int mod_ld,
                       int gate_off, int chunk_len, int M, int N, int K, const GemmWork& w,
-                      hipStream_t s) {
-  run_gemm(A, Bt, M, N, K, w, EpiGatedResid{h, mod, mod_ld, gate_off, chunk_len, N}, s);
+                      hipStream_t s, const int* period) {
+  run_gemm(A, Bt, M, N, K, w, EpiGatedResid{h, mod, mod_ld, gate_off, chunk_len, N, period}, s);
 }
 template <typename T>
 void gemm_geglu(const T* A, const T* Bt, T* out, int M, int N, int K, const GemmWork& w,
@@ -1231,13 +1254,13 @@ hipError_t gemm_prepare() {
 
 #define FV_INSTANTIATE(T)                                                                        \
   template void gemm_bias_silu<T>(const T*, const T*, const float*, T*, int, int, int,           \
-                                  const GemmWork&, hipStream_t);                                 \
+                                  const GemmWork&, hipStream_t, const int*);                     \
   template void gemm_bias_f32<T>(const T*, const T*, const float*, float*, int, int, int,        \
-                                 const GemmWork&, hipStream_t);                                  \
+                                 const GemmWork&, hipStream_t, const int*);                      \
   template void gemm_qkv<T>(const T*, const T*, const QkvArgs<T>&, int, int, int,                \
                             const GemmWork&, hipStream_t);                                       \
   template void gemm_gated_resid<T>(const T*, const T*, float*, const float*, int, int, int,     \
-                                    int, int, int, const GemmWork&, hipStream_t);                \
+                                    int, int, int, const GemmWork&, hipStream_t, const int*);    \
   template void gemm_geglu<T>(const T*, const T*, T*, int, int, int, const GemmWork&,            \
                               hipStream_t);                                                      \
   template void gemm_gelu<T>(const T*, const T*, T*, int, int, int, const GemmWork&, hipStream_t); \

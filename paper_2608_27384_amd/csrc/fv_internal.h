@@ -180,20 +180,22 @@ struct QkvArgs {
   int tokens, n_q_heads, n_kv_heads, head_dim, S;
 };
 
+// skip (optional): a device flag; when it holds a nonzero value at run time
+// the launch computes nothing (its workgroups return at once).
 template <typename T>
 void gemm_bias_silu(const T* A, const T* Bt, const float* bias, T* out, int M, int N, int K,
-                    const GemmWork& w, hipStream_t s);
+                    const GemmWork& w, hipStream_t s, const int* skip = nullptr);
 template <typename T>
 void gemm_bias_f32(const T* A, const T* Bt, const float* bias, float* out, int M, int N, int K,
-                   const GemmWork& w, hipStream_t s);
+                   const GemmWork& w, hipStream_t s, const int* skip = nullptr);
 template <typename T>
 void gemm_qkv(const T* A, const T* Bt, const QkvArgs<T>& qa, int M, int N, int K,
               const GemmWork& w, hipStream_t s);
-// h[row][col] += mod[row / chunk_len][gate_off + col] * acc
+// h[row][col] += mod[film_row(row / chunk_len, *period)][gate_off + col] * acc
 template <typename T>
 void gemm_gated_resid(const T* A, const T* Bt, float* h, const float* mod, int mod_ld,
                       int gate_off, int chunk_len, int M, int N, int K, const GemmWork& w,
-                      hipStream_t s);
+                      hipStream_t s, const int* period = nullptr);
 // out[row][n] = gelu(acc_gate) * acc_up   (packed columns, N = 2F)
 template <typename T>
 void gemm_geglu(const T* A, const T* Bt, T* out, int M, int N, int K, const GemmWork& w,
@@ -214,14 +216,29 @@ int gemm_partials(const T* A, const T* Bt, int M, int N, int K, const GemmWork& 
                   hipStream_t s, bool* bf16_parts);
 
 // ------------------------------------------------------------ other kernels
+// FiLM maps shared across streams.  Chunk row cr (stream b, slot k, cr =
+// b K + k) normally reads its own row of the FiLM maps.  When every stream's
+// noise levels equal stream 0's bit for bit, identical rows are computed
+// once: the step's period flag then holds K and chunk row cr reads row
+// cr % K (stream 0's), else it holds 0.  Readers take the flag's address
+// (`period`, nullptr: no sharing) and load it once.
+__device__ __forceinline__ int film_period(const int* period) { return period ? *period : 0; }
+__device__ __forceinline__ int film_row(int cr, int per) { return per ? cr % per : cr; }
+
+// e[row] = timestep embedding of t[row]; with `period`, one workgroup also
+// sets the period flag for rows of K slots per stream (K if every row's t
+// equals, bit for bit, that of the same slot of stream 0, else 0).
 template <typename T>
-void launch_time_embed(const float* t, T* e, int rows, int width, hipStream_t s);
+void launch_time_embed(const float* t, T* e, int rows, int width, hipStream_t s,
+                       int* period = nullptr, int K = 0);
 // xs (optional, only where head_fusable): a copy of x for the fused Euler
-// update of launch_final_euler.
+// update of launch_final_euler.  `period` (here and below): the FiLM-row
+// sharing flag described above, or nullptr.
 template <typename T>
 void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, float* h,
                          const float* mod, int mod_ld, int chunk_len, float eps, T* u, int rows,
-                         int A, int W, hipStream_t s, float* xs = nullptr);
+                         int A, int W, hipStream_t s, float* xs = nullptr,
+                         const int* period = nullptr);
 // h += gate * sum_z part[z] (split order); then, if norm_off >= 0,
 // u = rmsnorm(h) (1 + scale) + shift with the modulation at norm_off.
 // part holds bf16 values when bf16_parts, else fp32.  [pf, pf + pf_bytes)
@@ -230,13 +247,14 @@ void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, f
 template <typename T>
 void launch_resid_norm(const void* part, bool bf16_parts, int ks, float* h, const float* mod,
                        int mod_ld, int gate_off, int norm_off, int chunk_len, float eps, T* u,
-                       int rows, int W, const void* pf, size_t pf_bytes, hipStream_t s);
+                       int rows, int W, const void* pf, size_t pf_bytes, hipStream_t s,
+                       const int* period = nullptr);
 template <typename T>
 void launch_adarms(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
-                   float eps, T* u, int rows, int W, hipStream_t s);
+                   float eps, T* u, int rows, int W, hipStream_t s, const int* period = nullptr);
 void launch_final(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
                   float eps, const float* w_out, const float* b_out, float* v, int rows, int W,
-                  int A, hipStream_t s);
+                  int A, hipStream_t s, const int* period = nullptr);
 // Destination of the Euler update fused into the velocity head (Algorithm 1:
 // x_k <- x_k - dt_k v_k, emit slot 0, shift, refill slot K-1): the caller's
 // buffer, the copy xs of it taken by the embedding at the start of the step,
@@ -257,7 +275,7 @@ bool head_fusable(int rows, int W, int A);
 // launch_euler_shift fused in (same rounding, same noise); v is not stored.
 void launch_final_euler(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
                         float eps, const float* w_out, const float* b_out, int rows, int W, int A,
-                        const EulerDest& eu, hipStream_t s);
+                        const EulerDest& eu, hipStream_t s, const int* period = nullptr);
 void launch_euler_shift(float* buffer, const float* t, const float* v, float* out,
                         const uint64_t* noise_state, uint32_t* ticket, int* n_valid, int B, int K,
                         int CA, hipStream_t s);
@@ -364,6 +382,8 @@ struct Handle {
   // scratch
   void* e = nullptr; void* hid = nullptr; void* cond = nullptr;  // T [Bmax*K][W]
   float* mod = nullptr;                                           // [Bmax*K][Nmod]
+  int* d_film_period = nullptr;   // FiLM-row sharing flag of the step (see film_row)
+  const int* film_per = nullptr;  // the flag the last velocity pass's readers took, or nullptr
   float* hres = nullptr;                                          // [Bmax*T][W]
   void* u = nullptr;                                              // T [Bmax*T][W]
   void* q = nullptr; void* o = nullptr;                           // T [Bmax*T][Hq*dh]
@@ -393,6 +413,8 @@ struct Handle {
   int mask_mode = FV_MASK_CHUNK_CAUSAL;
   float* mod_cache = nullptr;    // [Bmax*K][Nmod] FiLM maps of a static schedule
   float* t_cache = nullptr;      // [Bmax*K] the schedule itself
+  int* d_sched_period = nullptr;  // the schedule's FiLM-row sharing flag
+  const int* sched_per = nullptr; // the flag its readers take, or nullptr
   int sched_batch = 0;           // batch the cached schedule was made for (0: none)
   uint32_t* d_ticket = nullptr;
 

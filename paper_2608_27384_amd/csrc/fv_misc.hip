@@ -14,16 +14,25 @@ constexpr double kTwoPi = 6.283185307179586476925286766559;
 // -------------------------------------------------------- time embedding
 // e[row] = [sin(2 pi t / p_i) | cos(2 pi t / p_i)], p_i = 4e-3 * (4/4e-3)^(i/(W/2-1)),
 // evaluated in fp64 (the timestep embedding that drives FiLM, Appendix
-// "Model architecture").
+// "Model architecture").  With `period`, workgroup 0 also sets the FiLM-row
+// sharing flag: K when every stream's K noise levels equal stream 0's bit
+// for bit (equal t gives equal maps, so stream 0's rows serve all), else 0.
 template <typename T>
 __global__ void time_embed_kernel(const float* __restrict__ t, T* __restrict__ e, int rows,
-                                  int width) {
+                                  int width, int* __restrict__ period, int K) {
+  if (period && blockIdx.x == 0) {
+    int same = 1;
+    for (int r = K + (int)threadIdx.x; r < rows; r += blockDim.x)
+      same &= __float_as_uint(t[r]) == __float_as_uint(t[r % K]);
+    same = __syncthreads_and(same);
+    if (threadIdx.x == 0) *period = same ? K : 0;
+  }
   const int half = width / 2;
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= rows * half) return;
   const int row = idx / half, i = idx - row * half;
-  const double period = 4e-3 * pow(4.0 / 4e-3, (double)i / (double)(half - 1));
-  const double ang = kTwoPi * (double)t[row] / period;
+  const double p_i = 4e-3 * pow(4.0 / 4e-3, (double)i / (double)(half - 1));
+  const double ang = kTwoPi * (double)t[row] / p_i;
   double sv, cv;
   sincos(ang, &sv, &cv);
   e[(size_t)row * width + i] = from_f32<T>((float)sv);
@@ -53,7 +62,7 @@ template <typename T, int NC>
 __global__ __launch_bounds__(256) void embed_adarms_kernel(
     const float* __restrict__ x, const float* __restrict__ w_in, const float* __restrict__ b_in,
     float* __restrict__ h, const float* __restrict__ mod, int mod_ld, int chunk_len, float eps,
-    T* __restrict__ u, int rows, int A, int W) {
+    T* __restrict__ u, int rows, int A, int W, const int* __restrict__ period) {
   // thread t owns columns 4t + 1024 i (i < NC, W <= 1024 NC) of kEmbRows
   // rows; the modulation and the first weight batch are requested before
   // anything waits, and h stays in registers between the embedding and the
@@ -63,6 +72,7 @@ __global__ __launch_bounds__(256) void embed_adarms_kernel(
   __shared__ float sred[kEmbRows][4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int row0 = blockIdx.x * kEmbRows;
+  const int per = film_period(period);
   const f32x4 zero4 = f32x4{0.f, 0.f, 0.f, 0.f};
   f32x4 sv[NC][kEmbRows], bv[NC][kEmbRows], acc[NC][kEmbRows];
 #pragma unroll
@@ -73,7 +83,7 @@ __global__ __launch_bounds__(256) void embed_adarms_kernel(
 #pragma unroll
     for (int r = 0; r < kEmbRows; ++r) {
       const int row = min(row0 + r, rows - 1);
-      const float* sc = mod + (size_t)(row / chunk_len) * mod_ld;
+      const float* sc = mod + (size_t)film_row(row / chunk_len, per) * mod_ld;
       sv[i][r] = ok ? *reinterpret_cast<const f32x4*>(sc + c) : zero4;
       bv[i][r] = ok ? *reinterpret_cast<const f32x4*>(sc + W + c) : zero4;
       acc[i][r] = bias;
@@ -152,13 +162,15 @@ template <typename T>
 __global__ __launch_bounds__(256) void embed_adarms_small_kernel(
     const float* __restrict__ x, const float* __restrict__ w_in, const float* __restrict__ b_in,
     float* __restrict__ h, const float* __restrict__ mod, int mod_ld, int chunk_len, float eps,
-    T* __restrict__ u, int rows, int A, int W, float* __restrict__ xs) {
+    T* __restrict__ u, int rows, int A, int W, float* __restrict__ xs,
+    const int* __restrict__ period) {
   constexpr int R = kEmbSmallRows, AM = 32;
   __shared__ float sred[R][4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int row0 = blockIdx.x * R;
   const int c = min(4 * tid, W - 4);
   const bool own = 4 * tid < W;
+  const int per = film_period(period);
   float xv[R][AM];
   f32x4 wv[AM], sv[R], bv[R];
 #pragma unroll
@@ -166,7 +178,7 @@ __global__ __launch_bounds__(256) void embed_adarms_small_kernel(
     const int row = min(row0 + r, rows - 1);
 #pragma unroll
     for (int a = 0; a < AM; ++a) xv[r][a] = x[(size_t)row * A + min(a, A - 1)];
-    const float* sc = mod + (size_t)(row / chunk_len) * mod_ld;
+    const float* sc = mod + (size_t)film_row(row / chunk_len, per) * mod_ld;
     sv[r] = *reinterpret_cast<const f32x4*>(sc + c);
     bv[r] = *reinterpret_cast<const f32x4*>(sc + W + c);
   }
@@ -213,7 +225,7 @@ template <typename T>
 __global__ __launch_bounds__(256) void embed_adarms_rows_kernel(
     const float* __restrict__ x, const float* __restrict__ w_in, const float* __restrict__ b_in,
     float* __restrict__ h, const float* __restrict__ mod, int mod_ld, int chunk_len, float eps,
-    T* __restrict__ u, int rows, int A, int W, int rows_per_block) {
+    T* __restrict__ u, int rows, int A, int W, int rows_per_block, const int* __restrict__ period) {
   __shared__ float sx[32][kEmbRows];
   __shared__ float sred[kEmbRows][4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -225,6 +237,7 @@ __global__ __launch_bounds__(256) void embed_adarms_rows_kernel(
   for (int a = 0; a < 32; ++a)
     wv[a] = ok && a < A ? *reinterpret_cast<const f32x4*>(w_in + (size_t)a * W + c) : zero4;
   const f32x4 bias = ok ? *reinterpret_cast<const f32x4*>(b_in + c) : zero4;
+  const int per = film_period(period);
   const int rend = min(rows, (blockIdx.x + 1) * rows_per_block);
   for (int row0 = blockIdx.x * rows_per_block; row0 < rend; row0 += kEmbRows) {
     __syncthreads();  // previous batch done with sx and sred
@@ -261,7 +274,7 @@ __global__ __launch_bounds__(256) void embed_adarms_rows_kernel(
       if (row >= rend || !ok) break;
       const float tot = sred[r][0] + sred[r][1] + sred[r][2] + sred[r][3];
       const float rinv = 1.0f / sqrtf(tot / (float)W + eps);
-      const float* sc = mod + (size_t)(row / chunk_len) * mod_ld;
+      const float* sc = mod + (size_t)film_row(row / chunk_len, per) * mod_ld;
       const f32x4 sv = *reinterpret_cast<const f32x4*>(sc + c);
       const f32x4 bv = *reinterpret_cast<const f32x4*>(sc + W + c);
       store4<T>(u + (size_t)row * W + c, acc[r][0] * rinv * (1.0f + sv[0]) + bv[0],
@@ -308,10 +321,11 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const P* __restrict__ p
                                                          int mod_ld, int gate_off, int norm_off,
                                                          int chunk_len, float eps,
                                                          T* __restrict__ u, int rows, int W,
-                                                         const void* pf, size_t pf_bytes) {
+                                                         const void* pf, size_t pf_bytes,
+                                                         const int* __restrict__ period) {
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x;
-  const float* mrow = mod + (size_t)(row / chunk_len) * mod_ld;
+  const float* mrow = mod + (size_t)film_row(row / chunk_len, film_period(period)) * mod_ld;
   const int nrm = norm_off >= 0 ? norm_off : 0;
   typename RawPart<P>::type pr[NQ][KSM];
   f32x4 g[NQ], hv[NQ], svq[NQ], bvq[NQ];
@@ -367,13 +381,15 @@ template <typename T>
 __global__ __launch_bounds__(256) void adarms_kernel(const float* __restrict__ h,
                                                      const float* __restrict__ mod, int mod_ld,
                                                      int scale_off, int chunk_len, float eps,
-                                                     T* __restrict__ u, int rows, int W) {
+                                                     T* __restrict__ u, int rows, int W,
+                                                     const int* __restrict__ period) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= rows) return;
   constexpr int NV = 2048 / 256;  // 4-float groups per lane for W <= 2048
   const float* hr = h + (size_t)row * W;
-  const float* sc = mod + (size_t)(row / chunk_len) * mod_ld + scale_off;
+  const float* sc =
+      mod + (size_t)film_row(row / chunk_len, film_period(period)) * mod_ld + scale_off;
   f32x4 x[NV], sv[NV], bv[NV];
 #pragma unroll
   for (int i = 0; i < NV; ++i) {  // all loads of the row first
@@ -415,7 +431,7 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ h,
                                                     const float* __restrict__ w_out,
                                                     const float* __restrict__ b_out,
                                                     float* __restrict__ v, int rows, int W,
-                                                    int A) {
+                                                    int A, const int* __restrict__ period) {
   extern __shared__ float smem[];  // su [kFinalRows][W], sp [parts][kFinalRows][A]
   float* su = smem;
   float* sp = su + kFinalRows * W;
@@ -424,7 +440,8 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ h,
   {
     const int row = min(row0 + wave, rows - 1);
     const float* hr = h + (size_t)row * W;
-    const float* sc = mod + (size_t)(row / chunk_len) * mod_ld + scale_off;
+    const float* sc =
+        mod + (size_t)film_row(row / chunk_len, film_period(period)) * mod_ld + scale_off;
     constexpr int NPL = kMaxW / 64;
     float hv[NPL], sv[NPL], bv[NPL];
 #pragma unroll
@@ -585,7 +602,8 @@ __global__ __launch_bounds__(256) void final_small_kernel(const float* __restric
                                                           const float* __restrict__ w_out,
                                                           const float* __restrict__ b_out,
                                                           float* __restrict__ v, int rows, int W,
-                                                          int A, EulerDest eu) {
+                                                          int A, EulerDest eu,
+                                                          const int* __restrict__ period) {
   constexpr int R = kFinalSmallRows, NPL = 16, KR = 32;
   __shared__ __attribute__((aligned(16))) float su[R][1024];
   __shared__ f32x4 sp[4][R][8];
@@ -621,7 +639,8 @@ __global__ __launch_bounds__(256) void final_small_kernel(const float* __restric
     wv[j] = *reinterpret_cast<const f32x4*>(w_out + (size_t)min(k0 + j, W - 1) * A + qa);
   const int row = min(row0 + wave, rows - 1);
   const float* hr = h + (size_t)row * W;
-  const float* sc = mod + (size_t)(row / chunk_len) * mod_ld + scale_off;
+  const float* sc =
+      mod + (size_t)film_row(row / chunk_len, film_period(period)) * mod_ld + scale_off;
   float hv[NPL], sv[NPL], bv[NPL];
 #pragma unroll
   for (int i = 0; i < NPL; ++i) {
@@ -684,7 +703,8 @@ __global__ __launch_bounds__(512) void final_rows_kernel(const float* __restrict
                                                          const float* __restrict__ w_out,
                                                          const float* __restrict__ b_out,
                                                          float* __restrict__ v, int rows, int W,
-                                                         int A, int rows_per_block) {
+                                                         int A, int rows_per_block,
+                                                         const int* __restrict__ period) {
   constexpr int R = kFinalRowsBig, KR = 64, NPL = 1024 / 64;
   extern __shared__ float smem[];  // su [R][W], sp [parts][R][A]
   float* su = smem;
@@ -697,12 +717,13 @@ __global__ __launch_bounds__(512) void final_rows_kernel(const float* __restrict
   float wr[KR];
 #pragma unroll
   for (int j = 0; j < KR; ++j) wr[j] = part < parts && k0 + j < k1 ? w_out[(size_t)(k0 + j) * A + a] : 0.f;
+  const int per = film_period(period);
   const int rend = min(rows, (blockIdx.x + 1) * rows_per_block);
   for (int row0 = blockIdx.x * rows_per_block; row0 < rend; row0 += R) {
     {
       const int row = min(row0 + wave, rend - 1);
       const float* hr = h + (size_t)row * W;
-      const float* sc = mod + (size_t)(row / chunk_len) * mod_ld + scale_off;
+      const float* sc = mod + (size_t)film_row(row / chunk_len, per) * mod_ld + scale_off;
       float hv[NPL], sv[NPL], bv[NPL];
 #pragma unroll
       for (int i = 0; i < NPL; ++i) {
@@ -927,10 +948,11 @@ __global__ __launch_bounds__(256) void prefix_copy_kernel(const T* __restrict__ 
 }  // namespace
 
 template <typename T>
-void launch_time_embed(const float* t, T* e, int rows, int width, hipStream_t s) {
+void launch_time_embed(const float* t, T* e, int rows, int width, hipStream_t s, int* period,
+                       int K) {
   const int n = rows * (width / 2);
   hipLaunchKernelGGL((time_embed_kernel<T>), dim3((n + 255) / 256), dim3(256), 0, s, t, e, rows,
-                     width);
+                     width, period, K);
 }
 
 bool head_fusable(int rows, int W, int A) {
@@ -940,38 +962,39 @@ bool head_fusable(int rows, int W, int A) {
 template <typename T>
 void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, float* h,
                          const float* mod, int mod_ld, int chunk_len, float eps, T* u, int rows,
-                         int A, int W, hipStream_t s, float* xs) {
+                         int A, int W, hipStream_t s, float* xs, const int* period) {
   if (rows >= kManyRows && W <= 1024 && A <= 32) {
     const int rpb = kEmbRows * std::max(1, rows / (kEmbRows * kRowBlocks));
     hipLaunchKernelGGL((embed_adarms_rows_kernel<T>), dim3((rows + rpb - 1) / rpb), dim3(256), 0, s,
-                       x, w_in, b_in, h, mod, mod_ld, chunk_len, eps, u, rows, A, W, rpb);
+                       x, w_in, b_in, h, mod, mod_ld, chunk_len, eps, u, rows, A, W, rpb, period);
     return;
   }
   if (W <= 1024 && W % 4 == 0 && A <= 32) {
     hipLaunchKernelGGL((embed_adarms_small_kernel<T>), dim3((rows + kEmbSmallRows - 1) / kEmbSmallRows),
                        dim3(256), 0, s, x, w_in, b_in, h, mod, mod_ld, chunk_len, eps, u, rows, A, W,
-                       xs);
+                       xs, period);
     return;
   }
   const dim3 grid((rows + kEmbRows - 1) / kEmbRows);
   if (W <= 1024)
     hipLaunchKernelGGL((embed_adarms_kernel<T, 1>), grid, dim3(256), 0, s, x, w_in, b_in, h, mod,
-                       mod_ld, chunk_len, eps, u, rows, A, W);
+                       mod_ld, chunk_len, eps, u, rows, A, W, period);
   else
     hipLaunchKernelGGL((embed_adarms_kernel<T, 2>), grid, dim3(256), 0, s, x, w_in, b_in, h, mod,
-                       mod_ld, chunk_len, eps, u, rows, A, W);
+                       mod_ld, chunk_len, eps, u, rows, A, W, period);
 }
 
 template <typename T>
 void launch_resid_norm(const void* part, bool bf16_parts, int ks, float* h, const float* mod,
                        int mod_ld, int gate_off, int norm_off, int chunk_len, float eps, T* u,
-                       int rows, int W, const void* pf, size_t pf_bytes, hipStream_t s) {
+                       int rows, int W, const void* pf, size_t pf_bytes, hipStream_t s,
+                       const int* period) {
   // split slots (power of two >= ks, at most 8) and column groups per thread
   const int ksm = ks <= 2 ? 2 : ks <= 4 ? 4 : 8;
   const int nq = W <= 1024 ? 1 : 2;
   auto go = [&](auto kern, const auto* pp) {
     hipLaunchKernelGGL(kern, dim3(rows), dim3(256), 0, s, pp, ks, h, mod, mod_ld, gate_off,
-                       norm_off, chunk_len, eps, u, rows, W, pf, pf_bytes);
+                       norm_off, chunk_len, eps, u, rows, W, pf, pf_bytes, period);
   };
 #define FV_RN(P, KSM, NQ) go(resid_norm_kernel<T, P, KSM, NQ>, static_cast<const P*>(part))
 #define FV_RN_Q(P, KSM) (nq == 1 ? FV_RN(P, KSM, 1) : FV_RN(P, KSM, 2))
@@ -987,39 +1010,39 @@ void launch_resid_norm(const void* part, bool bf16_parts, int ks, float* h, cons
 
 template <typename T>
 void launch_adarms(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
-                   float eps, T* u, int rows, int W, hipStream_t s) {
+                   float eps, T* u, int rows, int W, hipStream_t s, const int* period) {
   hipLaunchKernelGGL((adarms_kernel<T>), dim3((rows + 3) / 4), dim3(256), 0, s, h, mod, mod_ld,
-                     scale_off, chunk_len, eps, u, rows, W);
+                     scale_off, chunk_len, eps, u, rows, W, period);
 }
 
 void launch_final(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
                   float eps, const float* w_out, const float* b_out, float* v, int rows, int W,
-                  int A, hipStream_t s) {
+                  int A, hipStream_t s, const int* period) {
   const size_t lds = (size_t)(kFinalRows * W + 256 * kFinalRows) * sizeof(float);
   if (rows >= kManyRows && W <= 1024 && W % 4 == 0 && A <= 32 && 4 * A <= 512 &&
       ((((W + 512 / A - 1) / (512 / A)) + 3) & ~3) <= 64) {
     const int rpb = kFinalRowsBig * std::max(1, rows / (kFinalRowsBig * kRowBlocks));
     const size_t lds2 = (size_t)(kFinalRowsBig * W + 512 * kFinalRowsBig) * sizeof(float);
     hipLaunchKernelGGL(final_rows_kernel, dim3((rows + rpb - 1) / rpb), dim3(512), lds2, s, h, mod,
-                       mod_ld, scale_off, chunk_len, eps, w_out, b_out, v, rows, W, A, rpb);
+                       mod_ld, scale_off, chunk_len, eps, w_out, b_out, v, rows, W, A, rpb, period);
     return;
   }
   if (W <= 1024 && A <= 32 && A % 4 == 0) {
     hipLaunchKernelGGL(final_small_kernel<false>, dim3((rows + kFinalSmallRows - 1) / kFinalSmallRows),
                        dim3(256), 0, s, h, mod, mod_ld, scale_off, chunk_len, eps, w_out, b_out, v,
-                       rows, W, A, EulerDest{});
+                       rows, W, A, EulerDest{}, period);
     return;
   }
   hipLaunchKernelGGL(final_kernel, dim3((rows + kFinalRows - 1) / kFinalRows), dim3(256), lds, s, h, mod, mod_ld,
-                     scale_off, chunk_len, eps, w_out, b_out, v, rows, W, A);
+                     scale_off, chunk_len, eps, w_out, b_out, v, rows, W, A, period);
 }
 
 void launch_final_euler(const float* h, const float* mod, int mod_ld, int scale_off, int chunk_len,
                         float eps, const float* w_out, const float* b_out, int rows, int W, int A,
-                        const EulerDest& eu, hipStream_t s) {
+                        const EulerDest& eu, hipStream_t s, const int* period) {
   hipLaunchKernelGGL(final_small_kernel<true>, dim3((rows + kFinalSmallRows - 1) / kFinalSmallRows),
                      dim3(256), 0, s, h, mod, mod_ld, scale_off, chunk_len, eps, w_out, b_out,
-                     nullptr, rows, W, A, eu);
+                     nullptr, rows, W, A, eu, period);
 }
 
 void launch_euler_shift(float* buffer, const float* t, const float* v, float* out,
@@ -1062,24 +1085,24 @@ void launch_prefix_copy(const T* k, const T* v, int L, int B, int src_batch, int
                      dh, karena, vtarena, Bmax, S, len);
 }
 
-template void launch_time_embed<bf16_t>(const float*, bf16_t*, int, int, hipStream_t);
-template void launch_time_embed<float>(const float*, float*, int, int, hipStream_t);
+template void launch_time_embed<bf16_t>(const float*, bf16_t*, int, int, hipStream_t, int*, int);
+template void launch_time_embed<float>(const float*, float*, int, int, hipStream_t, int*, int);
 template void launch_embed_adarms<bf16_t>(const float*, const float*, const float*, float*,
                                           const float*, int, int, float, bf16_t*, int, int, int,
-                                          hipStream_t, float*);
+                                          hipStream_t, float*, const int*);
 template void launch_embed_adarms<float>(const float*, const float*, const float*, float*,
                                          const float*, int, int, float, float*, int, int, int,
-                                         hipStream_t, float*);
+                                         hipStream_t, float*, const int*);
 template void launch_resid_norm<bf16_t>(const void*, bool, int, float*, const float*, int, int,
                                         int, int, float, bf16_t*, int, int, const void*, size_t,
-                                        hipStream_t);
+                                        hipStream_t, const int*);
 template void launch_resid_norm<float>(const void*, bool, int, float*, const float*, int, int,
                                        int, int, float, float*, int, int, const void*, size_t,
-                                       hipStream_t);
+                                       hipStream_t, const int*);
 template void launch_adarms<bf16_t>(const float*, const float*, int, int, int, float, bf16_t*,
-                                    int, int, hipStream_t);
+                                    int, int, hipStream_t, const int*);
 template void launch_adarms<float>(const float*, const float*, int, int, int, float, float*, int,
-                                   int, hipStream_t);
+                                   int, hipStream_t, const int*);
 template void launch_prefix_copy<bf16_t>(const bf16_t*, const bf16_t*, int, int, int, int, int,
                                          int, bf16_t*, bf16_t*, int, int, const int*, hipStream_t);
 template void launch_prefix_copy<float>(const float*, const float*, int, int, int, int, int, int,

@@ -175,35 +175,57 @@ int attn_split(const Handle* h, int B) {
 #define FV_PREFETCH 1
 #endif
 
+// per: the FiLM-row sharing flag the maps' readers take (film_row), or nullptr.
 template <typename T>
-void resid_block(Handle* h, const float* mod, const T* A, const T* Bt, int K, int gate_off,
-                 int norm_off, int rowsT, hipStream_t s, const void* next_w = nullptr,
-                 size_t next_bytes = 0) {
+void resid_block(Handle* h, const float* mod, const int* per, const T* A, const T* Bt, int K,
+                 int gate_off, int norm_off, int rowsT, hipStream_t s,
+                 const void* next_w = nullptr, size_t next_bytes = 0) {
   const int W = h->W;
   bool bf16_parts = false;
   const int ks = gemm_partials<T>(A, Bt, rowsT, W, K, h->gw, s, &bf16_parts);
   if (ks <= 1)
-    gemm_gated_resid<T>(A, Bt, h->hres, mod, h->Nmod, gate_off, h->C, rowsT, W, K, h->gw, s);
+    gemm_gated_resid<T>(A, Bt, h->hres, mod, h->Nmod, gate_off, h->C, rowsT, W, K, h->gw, s, per);
   if (ks > 1) {
     launch_resid_norm<T>(h->gw.ws, bf16_parts, ks, h->hres, mod, h->Nmod, gate_off, norm_off,
                          h->C, h->cfg.rms_eps, (T*)h->u, rowsT, W,
-                         FV_PREFETCH ? next_w : nullptr, next_bytes, s);
+                         FV_PREFETCH ? next_w : nullptr, next_bytes, s, per);
   } else {
     if (norm_off >= 0)
       launch_adarms<T>(h->hres, mod, h->Nmod, norm_off, h->C, h->cfg.rms_eps, (T*)h->u, rowsT,
-                       W, s);
+                       W, s, per);
   }
+}
+
+// Time-MLP and FiLM-map GEMM of rows [r0, r0 + n) of the time embedding
+// (skip: a flag that makes every launch return at once when set, or nullptr).
+template <typename T>
+void film_rows(Handle* h, int r0, int n, float* mod, hipStream_t s, const int* skip) {
+  const int W = h->W;
+  const size_t o = (size_t)r0 * W;
+  gemm_bias_silu<T>((T*)h->e + o, (T*)h->w_t1, h->b_t1, (T*)h->hid + o, n, W, W, h->gw, s, skip);
+  gemm_bias_silu<T>((T*)h->hid + o, (T*)h->w_t2, h->b_t2, (T*)h->cond + o, n, W, W, h->gw, s,
+                    skip);
+  gemm_bias_f32<T>((T*)h->cond + o, (T*)h->w_mod, h->b_mod, mod + (size_t)r0 * h->Nmod, n,
+                   h->Nmod, W, h->gw, s, skip);
 }
 
 // FiLM maps of every norm for noise levels t [B*K]: timestep embedding,
 // time-MLP, one GEMM for all (2L+1) [scale | shift | gate] maps -> mod.
+// With a sharing flag and several streams, the K rows of stream 0 are
+// computed and the rest only when some stream's noise levels differ from
+// stream 0's (the time embedding sets the flag; otherwise those launches
+// return at once, and the readers take stream 0's rows).  Returns the flag
+// for the readers, or nullptr when every row was computed.
 template <typename T>
-void enqueue_film_maps(Handle* h, const float* t, int B, float* mod, hipStream_t s) {
-  const int W = h->W, rowsK = B * h->K;
-  launch_time_embed<T>(t, (T*)h->e, rowsK, W, s);
-  gemm_bias_silu<T>((T*)h->e, (T*)h->w_t1, h->b_t1, (T*)h->hid, rowsK, W, W, h->gw, s);
-  gemm_bias_silu<T>((T*)h->hid, (T*)h->w_t2, h->b_t2, (T*)h->cond, rowsK, W, W, h->gw, s);
-  gemm_bias_f32<T>((T*)h->cond, (T*)h->w_mod, h->b_mod, mod, rowsK, h->Nmod, W, h->gw, s);
+const int* enqueue_film_maps(Handle* h, const float* t, int B, float* mod, hipStream_t s,
+                             int* flag) {
+  const int K = h->K, rowsK = B * K;
+  if (B <= 1) flag = nullptr;
+  launch_time_embed<T>(t, (T*)h->e, rowsK, h->W, s, flag, K);
+  film_rows<T>(h, 0, flag ? K : rowsK, mod, s, nullptr);
+  if (!flag) return nullptr;
+  film_rows<T>(h, K, rowsK - K, mod, s, flag);
+  return flag;
 }
 
 // pf: the weights the next kernels read, pulled into the memory-side cache by
@@ -221,21 +243,26 @@ AttnArgs attn_args(const Handle* h, const void* kar, const void* var, int B, int
 // that takes it, the Euler update, emission, shift and refill run inside the
 // velocity head (the embedding keeps a copy of the buffer in h->v, which the
 // fused head reads instead of v); returns whether it did.
+// `share_film`: streams whose noise levels equal stream 0's take stream 0's
+// FiLM rows (enqueue_film_maps); off where every row of h->mod must be filled.
+// The static-schedule maps were made the same way (their own flag).
 template <typename T>
 bool enqueue_forward(Handle* h, const float* buffer, const float* t, int B, float* v_out,
                      int n_layers_run, hipStream_t s, const float* mod_cached,
-                     const EulerDest* eu) {
+                     const EulerDest* eu, bool share_film) {
   const int W = h->W, rowsT = B * h->T;
   const int Nmod = h->Nmod;
   const size_t layer_elems = (size_t)h->Bmax * h->Hkv * h->S * h->dh;
   const bool fuse = eu && n_layers_run == h->L && head_fusable(rowsT, W, h->A);
   const float* mod = mod_cached;
+  const int* per = mod_cached ? h->sched_per : nullptr;
   if (!mod) {
-    enqueue_film_maps<T>(h, t, B, h->mod, s);
+    per = enqueue_film_maps<T>(h, t, B, h->mod, s, share_film ? h->d_film_period : nullptr);
     mod = h->mod;
   }
+  h->film_per = per;
   launch_embed_adarms<T>(buffer, h->w_in, h->b_in, h->hres, mod, Nmod, h->C, h->cfg.rms_eps,
-                         (T*)h->u, rowsT, h->A, W, s, fuse ? h->v : nullptr);
+                         (T*)h->u, rowsT, h->A, W, s, fuse ? h->v : nullptr, per);
   const int n_split = attn_split(h, B);
   for (int l = 0; l < n_layers_run; ++l) {
     T* kar = (T*)h->karena + l * layer_elems;
@@ -251,27 +278,27 @@ bool enqueue_forward(Handle* h, const float* buffer, const float* t, int B, floa
     launch_attention<T>(aa, s);
     // (no prefetch of the gate/up weights here: the reduction would wait
     // for 16.8 MB of loads, batch-1 step 1433 -> 1415 us without it)
-    resid_block<T>(h, mod, (const T*)h->o, (const T*)h->wo[l], h->Hq * h->dh,
+    resid_block<T>(h, mod, per, (const T*)h->o, (const T*)h->wo[l], h->Hq * h->dh,
                    n_attn * 3 * W + 2 * W, n_mlp * 3 * W, rowsT, s);
     if (h->cfg.mlp_gated)
       gemm_geglu<T>((T*)h->u, (const T*)h->wgu[l], (T*)h->m, rowsT, h->Ngu, W, h->gw, s);
     else
       gemm_gelu<T>((T*)h->u, (const T*)h->wgu[l], (T*)h->m, rowsT, h->Ngu, W, h->gw, s);
     const int next_norm = l + 1 < h->L ? 2 * (l + 1) * 3 * W : -1;
-    resid_block<T>(h, mod, (const T*)h->m, (const T*)h->wd[l], h->F, n_mlp * 3 * W + 2 * W,
-                   next_norm, rowsT, s, l + 1 < h->L ? h->wqkv[l + 1] : nullptr,
-                   (size_t)h->Nqkv * W * h->esz);
+    resid_block<T>(h, mod, per, (const T*)h->m, (const T*)h->wd[l], h->F,
+                   n_mlp * 3 * W + 2 * W, next_norm, rowsT, s,
+                   l + 1 < h->L ? h->wqkv[l + 1] : nullptr, (size_t)h->Nqkv * W * h->esz);
   }
   if (fuse) {
     EulerDest d = *eu;
     d.xs = h->v;
     launch_final_euler(h->hres, mod, Nmod, 6 * h->L * W, h->C, h->cfg.rms_eps, h->w_out,
-                       h->b_out, rowsT, W, h->A, d, s);
+                       h->b_out, rowsT, W, h->A, d, s, per);
     return true;
   }
   if (v_out)
     launch_final(h->hres, mod, Nmod, 6 * h->L * W, h->C, h->cfg.rms_eps, h->w_out, h->b_out,
-                 v_out, rowsT, W, h->A, s);
+                 v_out, rowsT, W, h->A, s, per);
   return false;
 }
 
@@ -283,7 +310,7 @@ void proj_gemm_only(Handle* h, const T* A, const T* Bt, int K, int gate_off, int
   bool bf16_parts = false;
   if (gemm_partials<T>(A, Bt, rowsT, h->W, K, h->gw, s, &bf16_parts) <= 1)
     gemm_gated_resid<T>(A, Bt, h->hres, h->mod, h->Nmod, gate_off, h->C, rowsT, h->W, K, h->gw,
-                        s);
+                        s, h->film_per);
 }
 
 // The FiLM norm that follows a projection, alone: the split-K reduction with
@@ -297,10 +324,10 @@ void proj_norm_only(Handle* h, int K, int gate_off, int norm_off, int rowsT, hip
   if (p.ks > 1)
     launch_resid_norm<T>(h->gw.ws, gemm_partials_bf16(p, h->bf16), p.ks, h->hres, h->mod, h->Nmod,
                          gate_off, norm_off, h->C, h->cfg.rms_eps, (T*)h->u, rowsT, h->W,
-                         FV_PREFETCH ? pf : nullptr, pf_bytes, s);
+                         FV_PREFETCH ? pf : nullptr, pf_bytes, s, h->film_per);
   else if (norm_off >= 0)
     launch_adarms<T>(h->hres, h->mod, h->Nmod, norm_off, h->C, h->cfg.rms_eps, (T*)h->u, rowsT,
-                     h->W, s);
+                     h->W, s, h->film_per);
 }
 
 template <typename T>
@@ -332,8 +359,15 @@ void run_stage(Handle* h, int stage, int l, hipStream_t s) {
       break;
   }
   switch (stage) {
-    case 0:
-      gemm_bias_f32<T>((T*)h->cond, (T*)h->w_mod, h->b_mod, h->mod, rowsK, h->Nmod, W, h->gw, s);
+    case 0:  // the FiLM-map GEMM as the last velocity pass ran it
+      if (h->film_per) {
+        gemm_bias_f32<T>((T*)h->cond, (T*)h->w_mod, h->b_mod, h->mod, h->K, h->Nmod, W, h->gw, s);
+        const size_t o = (size_t)h->K * W;
+        gemm_bias_f32<T>((T*)h->cond + o, (T*)h->w_mod, h->b_mod, h->mod + (size_t)h->K * h->Nmod,
+                         rowsK - h->K, h->Nmod, W, h->gw, s, h->film_per);
+      } else {
+        gemm_bias_f32<T>((T*)h->cond, (T*)h->w_mod, h->b_mod, h->mod, rowsK, h->Nmod, W, h->gw, s);
+      }
       break;
     case 1: {
       QkvArgs<T> qa{(T*)h->q, kar, var, h->rcos, h->rsin, h->d_len, h->T, h->Hq, h->Hkv,
@@ -350,14 +384,14 @@ void run_stage(Handle* h, int stage, int l, hipStream_t s) {
       break;
     }
     case 6: {
-      resid_block<T>(h, h->mod, (const T*)h->o, (const T*)h->wo[l], h->Hq * h->dh,
+      resid_block<T>(h, h->mod, h->film_per, (const T*)h->o, (const T*)h->wo[l], h->Hq * h->dh,
                      n_attn * 3 * W + 2 * W, n_mlp * 3 * W, rowsT, s);
       break;
     }
     case 7: {
       const int next_norm = l + 1 < h->L ? 2 * (l + 1) * 3 * W : -1;
-      resid_block<T>(h, h->mod, (const T*)h->m, (const T*)h->wd[l], h->F, n_mlp * 3 * W + 2 * W,
-                     next_norm, rowsT, s);
+      resid_block<T>(h, h->mod, h->film_per, (const T*)h->m, (const T*)h->wd[l], h->F,
+                     n_mlp * 3 * W + 2 * W, next_norm, rowsT, s);
       break;
     }
     default:
@@ -369,10 +403,12 @@ void run_stage(Handle* h, int stage, int l, hipStream_t s) {
 }
 
 bool forward(Handle* h, const float* buffer, const float* t, int B, float* v_out, int n_layers,
-             hipStream_t s, const float* mod_cached = nullptr, const EulerDest* eu = nullptr) {
+             hipStream_t s, const float* mod_cached = nullptr, const EulerDest* eu = nullptr,
+             bool share_film = true) {
   if (h->bf16)
-    return enqueue_forward<bf16_t>(h, buffer, t, B, v_out, n_layers, s, mod_cached, eu);
-  return enqueue_forward<float>(h, buffer, t, B, v_out, n_layers, s, mod_cached, eu);
+    return enqueue_forward<bf16_t>(h, buffer, t, B, v_out, n_layers, s, mod_cached, eu,
+                                   share_film);
+  return enqueue_forward<float>(h, buffer, t, B, v_out, n_layers, s, mod_cached, eu, share_film);
 }
 
 // One decode step (Algorithm 1): the velocity pass, then the Euler update,
@@ -385,11 +421,11 @@ void decode(Handle* h, float* buffer, const float* t, int B, float* out_chunk, h
                        h->C * h->A, s);
 }
 
-void film_maps(Handle* h, const float* t, int B, float* mod, hipStream_t s) {
-  if (h->bf16)
-    enqueue_film_maps<bf16_t>(h, t, B, mod, s);
-  else
-    enqueue_film_maps<float>(h, t, B, mod, s);
+// FiLM maps of a static schedule, rows shared across streams as in a step
+// (flag: the schedule's own sharing flag); returns the flag its readers take.
+const int* film_maps(Handle* h, const float* t, int B, float* mod, hipStream_t s, int* flag) {
+  if (h->bf16) return enqueue_film_maps<bf16_t>(h, t, B, mod, s, flag);
+  return enqueue_film_maps<float>(h, t, B, mod, s, flag);
 }
 
 void check_launch() {
@@ -816,9 +852,11 @@ fv_status fv_create(const fv_weights* w, const fv_cfg* cfg, fv_handle* out) {
     H.seq_t = static_cast<float*>(dalloc(h, (size_t)H.Bmax * 4));
     H.d_noise = static_cast<uint64_t*>(dalloc(h, 16));
     H.d_ticket = static_cast<uint32_t*>(dalloc(h, 4));
+    H.d_film_period = static_cast<int*>(dalloc(h, 4));
     const uint64_t ns[2] = {cfg->noise_seed, 0};
     FV_HIP(hipMemcpy(H.d_noise, ns, 16, hipMemcpyHostToDevice));
     FV_HIP(hipMemset(H.d_ticket, 0, 4));
+    FV_HIP(hipMemset(H.d_film_period, 0, 4));
     FV_HIP(hipDeviceSynchronize());
   });
   if (st != FV_OK) {
@@ -1160,12 +1198,13 @@ fv_status fv_set_schedule(fv_handle h, const float* t, void* stream) {
     if (!h->mod_cache) {
       h->mod_cache = static_cast<float*>(dalloc(h, (size_t)h->Bmax * h->K * h->Nmod * 4));
       h->t_cache = static_cast<float*>(dalloc(h, (size_t)h->Bmax * h->K * 4));
+      h->d_sched_period = static_cast<int*>(dalloc(h, 4));
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
     (void)hipGetLastError();
     const int B = h->batch;
     launch_copy_f32(h->t_cache, t, (size_t)B * h->K, s);
-    film_maps(h, h->t_cache, B, h->mod_cache, s);
+    h->sched_per = film_maps(h, h->t_cache, B, h->mod_cache, s, h->d_sched_period);
     check_launch();
     h->sched_batch = B;
   });
@@ -1270,7 +1309,7 @@ fv_status fv_debug_forward(fv_handle h, const float* buffer, const float* t, int
     activate_staged(h, s);
     (void)hipGetLastError();
     const int B = h->batch;
-    forward(h, buffer, t, B, nullptr, n_layers_run, s);
+    forward(h, buffer, t, B, nullptr, n_layers_run, s, nullptr, nullptr, false);  // every FiLM row
     launch_copy_f32(h_out, h->hres, (size_t)B * h->T * h->W, s);
     if (mod_out) launch_copy_f32(mod_out, h->mod, (size_t)B * h->K * h->Nmod, s);
     check_launch();

@@ -195,3 +195,30 @@ def test_sequential_decode_parity(name):
             assert rel_err(got[b], ref[b]) < tol(w)
     finally:
         case.close()
+
+
+@pytest.mark.parametrize("name", ["small_bf16_b3", "small_fp32_b2"])
+def test_velocity_parity_per_stream_noise_levels(name):
+    """FiLM rows are shared only when every stream's noise levels equal stream
+    0's bit for bit.  Passes alternate between one differing slot in the last
+    stream, the shared staircase, a different staircase per stream and the
+    first case again, so rows left over from an earlier pass are caught."""
+    w = synth.workload(name)
+    case = Case(w)
+    try:
+        base = synth.noise_levels_batched(w).astype(np.float32)
+        one = base.copy()
+        one[-1, w.n_chunks // 2] *= np.float32(0.5)
+        every = (base * (1.0 - 0.07 * np.arange(w.batch, dtype=np.float32))[:, None]).astype(
+            np.float32)
+        for label, t in (("one slot", one), ("shared", base), ("every stream", every),
+                         ("one slot again", one)):
+            case.t = np.ascontiguousarray(t)
+            case.td = dev(case.t)
+            v = case.gpu_velocity()
+            errs = [rel_err(v[b, k], ref[k]) for b in range(w.batch)
+                    for ref in [case.oracle_velocity(b)] for k in range(w.n_chunks)]
+            print(name, label, "max rel err", max(errs))
+            assert max(errs) < tol(w), (label, max(errs))
+    finally:
+        case.close()
