@@ -46,9 +46,9 @@ __global__ void time_embed_kernel(const float* __restrict__ t, T* __restrict__ e
 // of every row, reads w_in once for all rows in batches of independent
 // loads and keeps the x rows in LDS.
 constexpr int kEmbRows = 8;
-// Row counts from which the embedding and the velocity head switch to their
-// weights-in-registers variants, and the block count those aim for.
-constexpr int kManyRows = 4096, kRowBlocks = 512;
+// Row count from which the embedding and the velocity head switch to their
+// weights-in-registers variants.
+constexpr int kManyRows = 4096;
 
 __device__ __forceinline__ float block_sum_256(float v, float* red) {
   v = wave_sum(v);
@@ -220,17 +220,26 @@ __global__ __launch_bounds__(256) void embed_adarms_small_kernel(
 
 // Many rows (W <= 1024, A <= 32): thread t keeps its four columns of w_in in
 // registers and the block runs batches of kEmbRows rows through them, so
-// w_in is read once per block instead of once per batch.
+// w_in is read once per block instead of once per batch.  The kernel holds
+// more than 256 registers per lane, so one workgroup fits a CU, and the grid
+// is sized to one round of them (launch_embed_adarms).  The next batch's x is requested at the
+// start of a batch and its modulation rows right after its arithmetic, so
+// their latency hides behind the arithmetic and the row-sum barrier.  Two barriers per batch: the one after the row sums
+// also keeps the next batch's x out of sx until every wave has read it, and
+// the one after sx is written keeps the next row sums out of sred until the
+// current ones are read.
 template <typename T>
 __global__ __launch_bounds__(256) void embed_adarms_rows_kernel(
     const float* __restrict__ x, const float* __restrict__ w_in, const float* __restrict__ b_in,
     float* __restrict__ h, const float* __restrict__ mod, int mod_ld, int chunk_len, float eps,
     T* __restrict__ u, int rows, int A, int W, int rows_per_block, const int* __restrict__ period) {
-  __shared__ float sx[32][kEmbRows];
-  __shared__ float sred[kEmbRows][4];
+  constexpr int R = kEmbRows;
+  __shared__ __attribute__((aligned(16))) float sx[32][R];
+  __shared__ float sred[R][4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c = 4 * tid;
   const bool ok = c < W;
+  const int cc = min(c, W - 4);
   const f32x4 zero4 = f32x4{0.f, 0.f, 0.f, 0.f};
   f32x4 wv[32];
 #pragma unroll
@@ -238,48 +247,61 @@ __global__ __launch_bounds__(256) void embed_adarms_rows_kernel(
     wv[a] = ok && a < A ? *reinterpret_cast<const f32x4*>(w_in + (size_t)a * W + c) : zero4;
   const f32x4 bias = ok ? *reinterpret_cast<const f32x4*>(b_in + c) : zero4;
   const int per = film_period(period);
-  const int rend = min(rows, (blockIdx.x + 1) * rows_per_block);
-  for (int row0 = blockIdx.x * rows_per_block; row0 < rend; row0 += kEmbRows) {
-    __syncthreads();  // previous batch done with sx and sred
-    {  // entries a >= A are zero (their weights are zero too)
-      const int r = tid >> 5, a = tid & 31;
-      sx[a][r] = row0 + r < rend && a < A ? x[(size_t)(row0 + r) * A + a] : 0.f;
-    }
+  const int rbeg = blockIdx.x * rows_per_block;
+  const int rend = min(rows, rbeg + rows_per_block);
+  // x of a batch: thread (r, a) = (tid / 32, tid % 32) holds entry a of row
+  // r (entries a >= A are zero, and so are their weights)
+  const int xr_r = tid >> 5, xr_a = tid & 31;
+  auto load_x = [&](int row0) __attribute__((always_inline)) {
+    return row0 + xr_r < rend && xr_a < A ? x[(size_t)(row0 + xr_r) * A + xr_a] : 0.f;
+  };
+  float xr = load_x(rbeg);
+  for (int row0 = rbeg; row0 < rend; row0 += R) {
+    sx[xr_a][xr_r] = xr;
+    xr = load_x(row0 + R);
     __syncthreads();
-    f32x4 acc[kEmbRows];
+    f32x4 acc[R];
 #pragma unroll
-    for (int r = 0; r < kEmbRows; ++r) acc[r] = bias;
+    for (int r = 0; r < R; ++r) acc[r] = bias;
 #pragma unroll
     for (int a = 0; a < 32; ++a) {
+      const f32x4 x0 = *reinterpret_cast<const f32x4*>(&sx[a][0]);
+      const f32x4 x1 = *reinterpret_cast<const f32x4*>(&sx[a][4]);
 #pragma unroll
-      for (int r = 0; r < kEmbRows; ++r) acc[r] += sx[a][r] * wv[a];
+      for (int r = 0; r < 4; ++r) {
+        acc[r] += x0[r] * wv[a];
+        acc[4 + r] += x1[r] * wv[a];
+      }
       if ((a & 7) == 7) __builtin_amdgcn_sched_barrier(0);  // bounds the LDS reads in flight
     }
-    float ss[kEmbRows];
+    // the modulation rows, in flight during the stores and the row-sum barrier
+    f32x4 sv[R], bv[R];
 #pragma unroll
-    for (int r = 0; r < kEmbRows; ++r) {
-      ss[r] = acc[r][0] * acc[r][0] + acc[r][1] * acc[r][1] + acc[r][2] * acc[r][2] +
-              acc[r][3] * acc[r][3];
-      if (ok && row0 + r < rend) *reinterpret_cast<f32x4*>(h + (size_t)(row0 + r) * W + c) = acc[r];
+    for (int r = 0; r < R; ++r) {
+      const int row = min(row0 + r, rend - 1);
+      const float* sc = mod + (size_t)film_row(row / chunk_len, per) * mod_ld;
+      sv[r] = *reinterpret_cast<const f32x4*>(sc + cc);
+      bv[r] = *reinterpret_cast<const f32x4*>(sc + W + cc);
     }
 #pragma unroll
-    for (int r = 0; r < kEmbRows; ++r) {
-      const float v = wave_sum(ok ? ss[r] : 0.f);
+    for (int r = 0; r < R; ++r) {
+      const float ss = acc[r][0] * acc[r][0] + acc[r][1] * acc[r][1] + acc[r][2] * acc[r][2] +
+                       acc[r][3] * acc[r][3];
+      if (ok && row0 + r < rend) *reinterpret_cast<f32x4*>(h + (size_t)(row0 + r) * W + c) = acc[r];
+      const float v = wave_sum(ok ? ss : 0.f);
       if (lane == 0) sred[r][wave] = v;
     }
     __syncthreads();
 #pragma unroll
-    for (int r = 0; r < kEmbRows; ++r) {
+    for (int r = 0; r < R; ++r) {
       const int row = row0 + r;
       if (row >= rend || !ok) break;
       const float tot = sred[r][0] + sred[r][1] + sred[r][2] + sred[r][3];
       const float rinv = 1.0f / sqrtf(tot / (float)W + eps);
-      const float* sc = mod + (size_t)film_row(row / chunk_len, per) * mod_ld;
-      const f32x4 sv = *reinterpret_cast<const f32x4*>(sc + c);
-      const f32x4 bv = *reinterpret_cast<const f32x4*>(sc + W + c);
-      store4<T>(u + (size_t)row * W + c, acc[r][0] * rinv * (1.0f + sv[0]) + bv[0],
-                acc[r][1] * rinv * (1.0f + sv[1]) + bv[1], acc[r][2] * rinv * (1.0f + sv[2]) + bv[2],
-                acc[r][3] * rinv * (1.0f + sv[3]) + bv[3]);
+      store4<T>(u + (size_t)row * W + c, acc[r][0] * rinv * (1.0f + sv[r][0]) + bv[r][0],
+                acc[r][1] * rinv * (1.0f + sv[r][1]) + bv[r][1],
+                acc[r][2] * rinv * (1.0f + sv[r][2]) + bv[r][2],
+                acc[r][3] * rinv * (1.0f + sv[r][3]) + bv[r][3]);
     }
   }
 }
@@ -696,6 +718,13 @@ __global__ __launch_bounds__(256) void final_small_kernel(const float* __restric
 // contiguous slice (at most 64 entries) of column a of w_out in registers
 // and the block runs batches of 8 rows (one per wave) through it: w_out is
 // read once per block.  Slices are added in a fixed order, as in final_kernel.
+// One workgroup per CU and a grid of one round (launch_final); each wave
+// requests its next row (h, scale, shift) as soon as the current one is in
+// LDS, so the load latency hides behind the head's arithmetic.  Two barriers
+// per batch: the one after the head's partial sums also keeps the next
+// batch's rows out of su until every wave has read it, and the one after su
+// is written keeps the next partial sums out of sp until the current ones are
+// added.
 constexpr int kFinalRowsBig = 8;
 __global__ __launch_bounds__(512) void final_rows_kernel(const float* __restrict__ h,
                                                          const float* __restrict__ mod, int mod_ld,
@@ -707,10 +736,10 @@ __global__ __launch_bounds__(512) void final_rows_kernel(const float* __restrict
                                                          const int* __restrict__ period) {
   constexpr int R = kFinalRowsBig, KR = 64, NPL = 1024 / 64;
   extern __shared__ float smem[];  // su [R][W], sp [parts][R][A]
-  float* su = smem;
-  float* sp = su + R * W;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, tid = threadIdx.x;
   const int parts = 512 / A;
+  float* su = smem;
+  float* sp = su + R * W;
   const int part = tid / A, a = tid - part * A;
   const int kr = (((W + parts - 1) / parts) + 3) & ~3;  // multiple of 4, at most KR
   const int k0 = part * kr, k1 = min(W, k0 + kr);
@@ -718,32 +747,36 @@ __global__ __launch_bounds__(512) void final_rows_kernel(const float* __restrict
 #pragma unroll
   for (int j = 0; j < KR; ++j) wr[j] = part < parts && k0 + j < k1 ? w_out[(size_t)(k0 + j) * A + a] : 0.f;
   const int per = film_period(period);
-  const int rend = min(rows, (blockIdx.x + 1) * rows_per_block);
-  for (int row0 = blockIdx.x * rows_per_block; row0 < rend; row0 += R) {
-    {
-      const int row = min(row0 + wave, rend - 1);
-      const float* hr = h + (size_t)row * W;
-      const float* sc = mod + (size_t)film_row(row / chunk_len, per) * mod_ld + scale_off;
-      float hv[NPL], sv[NPL], bv[NPL];
+  const int rbeg = blockIdx.x * rows_per_block;
+  const int rend = min(rows, rbeg + rows_per_block);
+  float hv[NPL], sv[NPL], bv[NPL];
+  auto load_row = [&](int row0) __attribute__((always_inline)) {  // this wave's row of a batch
+    const int row = min(row0 + wave, rend - 1);
+    const float* hr = h + (size_t)row * W;
+    const float* sc = mod + (size_t)film_row(row / chunk_len, per) * mod_ld + scale_off;
 #pragma unroll
-      for (int i = 0; i < NPL; ++i) {
-        const int cc = lane + 64 * i;
-        hv[i] = cc < W ? hr[cc] : 0.f;
-        sv[i] = cc < W ? sc[cc] : 0.f;
-        bv[i] = cc < W ? sc[W + cc] : 0.f;
-      }
+    for (int i = 0; i < NPL; ++i) {
+      const int cc = min(lane + 64 * i, W - 1);
+      hv[i] = hr[cc];
+      sv[i] = sc[cc];
+      bv[i] = sc[W + cc];
+    }
+  };
+  if (rbeg < rend) load_row(rbeg);
+  for (int row0 = rbeg; row0 < rend; row0 += R) {
+    {
       float ss = 0.f;
 #pragma unroll
-      for (int i = 0; i < NPL; ++i) ss += hv[i] * hv[i];
+      for (int i = 0; i < NPL; ++i) ss += lane + 64 * i < W ? hv[i] * hv[i] : 0.f;
       ss = wave_sum(ss);
       const float rinv = 1.0f / sqrtf(ss / (float)W + eps);
-      __syncthreads();  // previous batch done with su and sp
 #pragma unroll
       for (int i = 0; i < NPL; ++i) {
         const int cc = lane + 64 * i;
         if (cc < W) su[wave * W + cc] = hv[i] * rinv * (1.0f + sv[i]) + bv[i];
       }
     }
+    if (row0 + R < rend) load_row(row0 + R);
     __syncthreads();
     if (part < parts) {
 #pragma unroll
@@ -964,7 +997,8 @@ void launch_embed_adarms(const float* x, const float* w_in, const float* b_in, f
                          const float* mod, int mod_ld, int chunk_len, float eps, T* u, int rows,
                          int A, int W, hipStream_t s, float* xs, const int* period) {
   if (rows >= kManyRows && W <= 1024 && A <= 32) {
-    const int rpb = kEmbRows * std::max(1, rows / (kEmbRows * kRowBlocks));
+    // one round of one workgroup per CU
+    const int rpb = kEmbRows * ((rows + kEmbRows * 256 - 1) / (kEmbRows * 256));
     hipLaunchKernelGGL((embed_adarms_rows_kernel<T>), dim3((rows + rpb - 1) / rpb), dim3(256), 0, s,
                        x, w_in, b_in, h, mod, mod_ld, chunk_len, eps, u, rows, A, W, rpb, period);
     return;
@@ -1021,7 +1055,8 @@ void launch_final(const float* h, const float* mod, int mod_ld, int scale_off, i
   const size_t lds = (size_t)(kFinalRows * W + 256 * kFinalRows) * sizeof(float);
   if (rows >= kManyRows && W <= 1024 && W % 4 == 0 && A <= 32 && 4 * A <= 512 &&
       ((((W + 512 / A - 1) / (512 / A)) + 3) & ~3) <= 64) {
-    const int rpb = kFinalRowsBig * std::max(1, rows / (kFinalRowsBig * kRowBlocks));
+    // one round of one workgroup per CU
+    const int rpb = kFinalRowsBig * ((rows + kFinalRowsBig * 256 - 1) / (kFinalRowsBig * 256));
     const size_t lds2 = (size_t)(kFinalRowsBig * W + 512 * kFinalRowsBig) * sizeof(float);
     hipLaunchKernelGGL(final_rows_kernel, dim3((rows + rpb - 1) / rpb), dim3(512), lds2, s, h, mod,
                        mod_ld, scale_off, chunk_len, eps, w_out, b_out, v, rows, W, A, rpb, period);
