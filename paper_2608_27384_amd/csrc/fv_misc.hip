@@ -714,17 +714,18 @@ __global__ __launch_bounds__(256) void final_small_kernel(const float* __restric
   if constexpr (EU) euler_finish(eu, rows / (eu.K * chunk_len), step);
 }
 
-// Many rows (W <= 1024, A <= 32): 512 threads; thread (part, a) keeps its
-// contiguous slice (at most 64 entries) of column a of w_out in registers
-// and the block runs batches of 8 rows (one per wave) through it: w_out is
-// read once per block.  Slices are added in a fixed order, as in final_kernel.
-// One workgroup per CU and a grid of one round (launch_final); each wave
-// requests its next row (h, scale, shift) as soon as the current one is in
-// LDS, so the load latency hides behind the head's arithmetic.  Two barriers
-// per batch: the one after the head's partial sums also keeps the next
-// batch's rows out of su until every wave has read it, and the one after su
-// is written keeps the next partial sums out of sp until the current ones are
-// added.
+// Many rows (W <= 1024, A <= 32, A % 4 == 0): 512 threads; thread (part, q)
+// keeps rows 16 part .. 16 part + 15 of w_out at outputs 4q .. 4q + 3 in
+// registers and the block runs batches of 8 rows (one per wave) through
+// them: w_out is read once per block, and every normalised value read from
+// LDS feeds four outputs.  The 8 parts of a wave are added across lanes
+// (lane bits 5, 4, 3) and the 8 waves in a fixed order.  One workgroup per
+// CU and a grid of one round (launch_final); each wave requests its next row
+// (h, scale, shift) as soon as the current one is in LDS, so the load latency
+// hides behind the head's arithmetic.  Two barriers per batch: the one after
+// the partial sums also keeps the next rows out of su until every wave has
+// read it, and the one after su is written keeps the next partial sums out
+// of sp until the current ones are added.
 constexpr int kFinalRowsBig = 8;
 __global__ __launch_bounds__(512) void final_rows_kernel(const float* __restrict__ h,
                                                          const float* __restrict__ mod, int mod_ld,
@@ -734,18 +735,19 @@ __global__ __launch_bounds__(512) void final_rows_kernel(const float* __restrict
                                                          float* __restrict__ v, int rows, int W,
                                                          int A, int rows_per_block,
                                                          const int* __restrict__ period) {
-  constexpr int R = kFinalRowsBig, KR = 64, NPL = 1024 / 64;
-  extern __shared__ float smem[];  // su [R][W], sp [parts][R][A]
+  constexpr int R = kFinalRowsBig, KS = 16, NPL = 1024 / 64;
+  __shared__ __attribute__((aligned(16))) float su[R][1024];  // zero past W
+  __shared__ f32x4 sp[8][R][8];                                 // [wave][row][quad]
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, tid = threadIdx.x;
-  const int parts = 512 / A;
-  float* su = smem;
-  float* sp = su + R * W;
-  const int part = tid / A, a = tid - part * A;
-  const int kr = (((W + parts - 1) / parts) + 3) & ~3;  // multiple of 4, at most KR
-  const int k0 = part * kr, k1 = min(W, k0 + kr);
-  float wr[KR];
+  const int q = tid & 7, part = tid >> 3;
+  const int qa = min(4 * q, A - 4);
+  const int k0 = KS * part;
+  f32x4 wr[KS];
 #pragma unroll
-  for (int j = 0; j < KR; ++j) wr[j] = part < parts && k0 + j < k1 ? w_out[(size_t)(k0 + j) * A + a] : 0.f;
+  for (int j = 0; j < KS; ++j)
+    wr[j] = k0 + j < W && 4 * q < A ? *reinterpret_cast<const f32x4*>(w_out + (size_t)(k0 + j) * A + qa)
+                                    : f32x4{0.f, 0.f, 0.f, 0.f};
+  const f32x4 bo = *reinterpret_cast<const f32x4*>(b_out + qa);
   const int per = film_period(period);
   const int rbeg = blockIdx.x * rows_per_block;
   const int rend = min(rows, rbeg + rows_per_block);
@@ -773,36 +775,34 @@ __global__ __launch_bounds__(512) void final_rows_kernel(const float* __restrict
 #pragma unroll
       for (int i = 0; i < NPL; ++i) {
         const int cc = lane + 64 * i;
-        if (cc < W) su[wave * W + cc] = hv[i] * rinv * (1.0f + sv[i]) + bv[i];
+        su[wave][cc] = cc < W ? hv[i] * rinv * (1.0f + sv[i]) + bv[i] : 0.f;
       }
     }
     if (row0 + R < rend) load_row(row0 + R);
     __syncthreads();
-    if (part < parts) {
 #pragma unroll
-      for (int r = 0; r < R; ++r) {
-        float acc = 0.f;
+    for (int r = 0; r < R; ++r) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int j = 0; j < KR; j += 4) {
-          // past the slice: zero weights; the LDS value is replaced too, as it
-          // may be any bit pattern (the allocation is large enough to read)
-          const f32x4 x4 = k0 + j < k1 ? *reinterpret_cast<const f32x4*>(su + r * W + k0 + j)
-                                       : f32x4{0.f, 0.f, 0.f, 0.f};
-          acc = fmaf(x4[0], wr[j], acc);
-          acc = fmaf(x4[1], wr[j + 1], acc);
-          acc = fmaf(x4[2], wr[j + 2], acc);
-          acc = fmaf(x4[3], wr[j + 3], acc);
-        }
-        sp[(part * R + r) * A + a] = acc;
+      for (int j = 0; j < KS; j += 4) {
+        const f32x4 x4 = *reinterpret_cast<const f32x4*>(&su[r][k0 + j]);
+        acc += x4[0] * wr[j];
+        acc += x4[1] * wr[j + 1];
+        acc += x4[2] * wr[j + 2];
+        acc += x4[3] * wr[j + 3];
       }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[e] = sum_lane_bits_543(acc[e]);
+      if (lane < 8) sp[wave][r][lane] = acc;
     }
     __syncthreads();
-    if (tid < R * A) {
-      const int r = tid / A, aa = tid - r * A;
-      if (row0 + r < rend) {
-        float tot = b_out[aa];
-        for (int p = 0; p < parts; ++p) tot += sp[(p * R + r) * A + aa];
-        v[(size_t)(row0 + r) * A + aa] = tot;
+    if (tid < R * 8) {
+      const int r = tid >> 3;
+      if (row0 + r < rend && 4 * q < A) {
+        f32x4 vv = bo;
+#pragma unroll
+        for (int w = 0; w < 8; ++w) vv += sp[w][r][q];
+        *reinterpret_cast<f32x4*>(v + (size_t)(row0 + r) * A + 4 * q) = vv;
       }
     }
   }
@@ -1053,12 +1053,10 @@ void launch_final(const float* h, const float* mod, int mod_ld, int scale_off, i
                   float eps, const float* w_out, const float* b_out, float* v, int rows, int W,
                   int A, hipStream_t s, const int* period) {
   const size_t lds = (size_t)(kFinalRows * W + 256 * kFinalRows) * sizeof(float);
-  if (rows >= kManyRows && W <= 1024 && W % 4 == 0 && A <= 32 && 4 * A <= 512 &&
-      ((((W + 512 / A - 1) / (512 / A)) + 3) & ~3) <= 64) {
+  if (rows >= kManyRows && W <= 1024 && W % 4 == 0 && A <= 32 && A % 4 == 0) {
     // one round of one workgroup per CU
     const int rpb = kFinalRowsBig * ((rows + kFinalRowsBig * 256 - 1) / (kFinalRowsBig * 256));
-    const size_t lds2 = (size_t)(kFinalRowsBig * W + 512 * kFinalRowsBig) * sizeof(float);
-    hipLaunchKernelGGL(final_rows_kernel, dim3((rows + rpb - 1) / rpb), dim3(512), lds2, s, h, mod,
+    hipLaunchKernelGGL(final_rows_kernel, dim3((rows + rpb - 1) / rpb), dim3(512), 0, s, h, mod,
                        mod_ld, scale_off, chunk_len, eps, w_out, b_out, v, rows, W, A, rpb, period);
     return;
   }
