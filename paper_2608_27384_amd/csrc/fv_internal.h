@@ -383,7 +383,7 @@ struct Handle {
   void* e = nullptr; void* hid = nullptr; void* cond = nullptr;  // T [Bmax*K][W]
   float* mod = nullptr;                                           // [Bmax*K][Nmod]
   int* d_film_period = nullptr;   // FiLM-row sharing flag of the step (see film_row)
-  const int* film_per = nullptr;  // the flag the last velocity pass's readers took, or nullptr
+  const int* film_per = nullptr;  // the flag of h->mod's rows after the last velocity pass, or nullptr
   float* hres = nullptr;                                          // [Bmax*T][W]
   void* u = nullptr;                                              // T [Bmax*T][W]
   void* q = nullptr; void* o = nullptr;                           // T [Bmax*T][Hq*dh]

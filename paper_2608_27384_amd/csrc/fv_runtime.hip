@@ -260,7 +260,7 @@ bool enqueue_forward(Handle* h, const float* buffer, const float* t, int B, floa
     per = enqueue_film_maps<T>(h, t, B, h->mod, s, share_film ? h->d_film_period : nullptr);
     mod = h->mod;
   }
-  h->film_per = per;
+  h->film_per = mod_cached ? nullptr : per;  // the flag that goes with h->mod (debug stages)
   launch_embed_adarms<T>(buffer, h->w_in, h->b_in, h->hres, mod, Nmod, h->C, h->cfg.rms_eps,
                          (T*)h->u, rowsT, h->A, W, s, fuse ? h->v : nullptr, per);
   const int n_split = attn_split(h, B);
