@@ -811,8 +811,8 @@ struct EpiGatedResid {
           const int idx = (q0 + q) * 64 + lane, rr = idx / C4, c4 = idx - rr * C4;
           const int row = min(row0 + 32 * i0 + rr, M - 1);
           hv[q] = *reinterpret_cast<const f32x4*>(hh + (size_t)row * ldh + col0 + 4 * c4);
-          gv[q] = *reinterpret_cast<const f32x4*>(mm + (size_t)film_row(row / chunk_len, per) * mod_ld +
-                                                  gate_off + col0 + 4 * c4);
+          const size_t mrow = (size_t)film_row(row / chunk_len, per) * mod_ld;
+          gv[q] = *reinterpret_cast<const f32x4*>(mm + mrow + gate_off + col0 + 4 * c4);
         }
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
