@@ -83,7 +83,7 @@ enum { FV_MASK_CHUNK_CAUSAL = 0, FV_MASK_ISOLATED = 1, FV_MASK_BIDIRECTIONAL = 2
  * Requirements (else FV_ERR_INVALID_ARG): every size >= 1 (max_prefix >= 0);
  * W % 128 == 0 and W <= 2048; dh in {64, 128, 192, 256}; F % 64 == 0 (F % 128
  * == 0 for the plain MLP); ((Hq + 2 Hkv) * dh) % 128 == 0; A <= 64;
- * K * C <= 4096; max_prefix + K * C <= 32768; max_batch <= 4096;
+ * K * C <= 4096; K <= 256; max_prefix + K * C <= 32768; max_batch <= 4096;
  * max_batch * K * C <= 262144; L * max_batch * Hkv <= 65535.
  */
 typedef struct {

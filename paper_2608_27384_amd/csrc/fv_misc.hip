@@ -810,12 +810,16 @@ __global__ __launch_bounds__(512) void final_rows_kernel(const float* __restrict
 
 // ------------------------------------------- Euler + emit + shift + refill
 // Thread (j, k) owns group j of 4 consecutive elements of the [C][A] chunk in
-// slot k of stream b; all K slots of a group live in one block.  Every thread
-// loads its slot and applies x'_k = x_k - dt_k v_k (rounded product, rounded
-// difference); after a barrier slot 0 writes the emitted chunk, slot k >= 1
-// writes buffer[k-1], and slot K-1 also writes fresh noise into buffer[K-1].
-// All loads precede the barrier and all stores follow it, so the in-place
-// shift has no race.  The last block to finish advances the step counter.
+// slot k of stream b; all K slots of a group live in one block.  A block
+// holds gpb = 256 / K consecutive groups; thread t takes slot t / gpb and
+// group t % gpb, so neighbouring lanes touch neighbouring groups (whole
+// 16-byte runs of a slot) and the fp64 refill of slot K-1 runs in one wave.
+// Every thread loads its slot and applies x'_k = x_k - dt_k v_k (rounded
+// product, rounded difference); after a barrier slot 0 writes the emitted
+// chunk, slot k >= 1 writes buffer[k-1], and slot K-1 also writes fresh noise
+// into buffer[K-1].  All loads precede the barrier and all stores follow it,
+// so the in-place shift has no race.  The last block to finish advances the
+// step counter.
 __global__ __launch_bounds__(256) void euler_shift_kernel(float* __restrict__ buf,
                                                           const float* __restrict__ t,
                                                           const float* __restrict__ v,
@@ -828,10 +832,10 @@ __global__ __launch_bounds__(256) void euler_shift_kernel(float* __restrict__ bu
 #pragma clang fp contract(off)
   const int groups = (CA + 3) >> 2;
   const int gpb = 256 / K;                      // element groups per block
-  const int k = threadIdx.x % K, jl = threadIdx.x / K;
+  const int k = threadIdx.x / gpb, jl = threadIdx.x % gpb;
   const int gid = blockIdx.x * gpb + jl;        // global group index over (b, j)
   const uint64_t seed = noise_state[0], step = noise_state[1];
-  const bool active = jl < gpb && gid < B * groups;
+  const bool active = k < K && gid < B * groups;
   float xn[4] = {0.f, 0.f, 0.f, 0.f};
   int b = 0, j = 0, e0 = 0, ne = 0;
   bool full = true;  // the popped slot holds a real chunk (not cold-start padding)

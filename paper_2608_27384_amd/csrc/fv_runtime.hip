@@ -145,6 +145,7 @@ void validate_cfg(const fv_cfg& c) {
     bad("(n_q_heads + 2 n_kv_heads) * head_dim must be a multiple of 128");
   if (c.action_dim > 64) bad("action_dim must be at most 64");
   if ((long)c.n_chunks * c.chunk_len > 4096) bad("n_chunks * chunk_len must be at most 4096");
+  if (c.n_chunks > 256) bad("n_chunks must be at most 256");  // one queue-update block per group
   if ((long)c.max_prefix + (long)c.n_chunks * c.chunk_len > 32768)
     bad("max_prefix + n_chunks * chunk_len must be at most 32768");
   if (c.max_batch > 4096) bad("max_batch must be at most 4096");

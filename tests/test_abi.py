@@ -61,7 +61,8 @@ def test_null_handle_and_null_arguments_are_rejected():
 
 @pytest.mark.parametrize("field,value", [
     ("n_kv_heads", 3), ("width", 96), ("head_dim", 48), ("head_dim", 512), ("mlp_dim", 100),
-    ("action_dim", 65), ("n_chunks", 0), ("max_batch", 0), ("dtype", 7), ("mlp_gated", 2),
+    ("action_dim", 65), ("n_chunks", 0), ("n_chunks", 257), ("max_batch", 0), ("dtype", 7),
+    ("mlp_gated", 2),
 ])
 def test_invalid_config_rejected_before_device_work(field, value):
     w = synth.workload("tiny_fp32")

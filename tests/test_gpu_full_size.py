@@ -84,7 +84,10 @@ def test_velocity_parity_batched64_all_streams():
 def test_velocity_parity_ragged_large_m():
     """9 streams of the batched workload: 4500 token rows, so the large-row
     GEMM tiles (256 rows) end in a partial tile of 148 rows, which belongs to
-    the last stream."""
+    the last stream.  Then one decode step, which at this many rows runs the
+    velocity head and the queue update as separate kernels: buffer and emitted
+    chunk bit for bit against the fp32 queue update of the GPU's own velocity,
+    refill against the oracle's Philox draw."""
     w = synth.workload("batched64").replace(name="batched9", batch=9)
     case = Case(w)
     try:
@@ -95,6 +98,20 @@ def test_velocity_parity_ragged_large_m():
             errs = [rel_err(v[b, k], ref[k]) for k in range(w.n_chunks)]
             _say(f"batched9 stream {b} (P={case.lens[b]}): max rel err {max(errs):.2e}")
             assert max(errs) < tol(w), (b, errs)
+        case.ex.set_noise_state(0, 5)
+        pre = host(case.xd).copy()
+        case.ex.decode_step(case.xd, case.td, case.out)
+        post, out = host(case.xd), host(case.out)
+        mism = 0
+        for b in range(w.batch):
+            z = oracle.gaussian_chunk(b, 5, w.chunk_len, w.action_dim)
+            new, ref_out = oracle.euler_emit_shift(pre[b], case.t[b], v[b], z, np.float32)
+            assert np.array_equal(out[b], ref_out), b
+            assert np.array_equal(post[b, :-1], new[:-1]), b
+            mism += int(np.count_nonzero(post[b, -1] != z))
+            assert np.max(np.abs(post[b, -1] - z)) <= 1e-6
+        _say(f"batched9 decode step: refill values differing from the oracle's draw: {mism}")
+        assert mism <= 2
     finally:
         case.close()
 

@@ -135,6 +135,46 @@ def test_bookkeeping_bit_exact(name):
         case.close()
 
 
+@pytest.mark.parametrize("name,K,C", [("tiny_fp32", 4, 8), ("small_bf16_b3", 3, 10),
+                                      ("tiny_fp32", 256, 2), ("small_fp32_b2", 255, 1)])
+def test_euler_shift_entry_point_bit_exact(name, K, C):
+    """fv_euler_shift, the separate queue-update kernel that the many-row
+    decode step also runs, on a caller-given velocity: the buffer and emitted
+    chunk equal, bit for bit, the fp32 queue update; the refill equals the
+    oracle's Philox draw; a stream still in cold start pops padding and emits
+    zeros; the valid-slot counts and the step counter advance.  Buffer
+    lengths K = 3 .. 256 (the queue-update blocks hold 256 / K element groups
+    of every slot, down to one group at K = 256)."""
+    w = synth.workload(name).replace(n_chunks=K, chunk_len=C)
+    case = Case(w, noise_seed=55)
+    try:
+        K = w.n_chunks
+        v = synth.perturbed(np.zeros_like(case.x), 5, "euler_v")
+        case.ex.set_noise_state(55, 3)
+        counts = [K - 1] + [K] * (w.batch - 1)
+        case.ex.set_valid_slots(counts)
+        pre = case.x.copy()
+        case.ex.euler_shift(case.xd, case.td, dev(v), case.out)
+        post, out = host(case.xd), host(case.out)
+        mism = 0
+        for b in range(w.batch):
+            z = oracle.gaussian_chunk(55 + b, 3, w.chunk_len, w.action_dim)
+            new, ref_out = oracle.euler_emit_shift(pre[b], case.t[b], v[b], z, np.float32)
+            if counts[b] < K:
+                assert not np.any(out[b]), "padding popped: nothing is emitted"
+            else:
+                assert np.array_equal(out[b], ref_out)
+            assert np.array_equal(post[b, :-1], new[:-1])
+            mism += int(np.count_nonzero(post[b, -1] != z))
+            assert np.max(np.abs(post[b, -1] - z)) <= 1e-6
+        print(f"{name}: refill values differing from the oracle's draw: {mism}")
+        assert mism <= 2  # fp64 libm ties only
+        assert case.ex.noise_state == (55, 4)
+        assert case.ex.valid_slots() == [K] * w.batch
+    finally:
+        case.close()
+
+
 def test_causality_bit_exact_on_gpu():
     """Perturbing chunks after k leaves the velocity of chunks <= k unchanged, bitwise."""
     w = synth.workload("small_bf16")
