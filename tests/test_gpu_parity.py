@@ -175,6 +175,41 @@ def test_euler_shift_entry_point_bit_exact(name, K, C):
         case.close()
 
 
+def test_fp32_many_rows():
+    """fp32 mode at 4800 token rows (24 streams of 10 chunks x 20 tokens,
+    ragged prefixes): the large-row fp32 GEMM tiles (256 x 128, the last one
+    partial), the many-row head and the separate queue update.  Velocities of
+    three streams against the oracle within 1e-4; one decode step, buffer and
+    emitted chunks bit for bit against the fp32 queue update of the GPU's own
+    velocity for every stream."""
+    w = synth.workload("small_fp32_b2").replace(name="fp32_rows", n_chunks=10, chunk_len=20,
+                                                 batch=24)
+    assert w.batch * w.tokens >= 4096
+    case = Case(w, noise_seed=9)
+    try:
+        v = case.gpu_velocity()
+        for b in (0, int(np.argmin(case.lens)), w.batch - 1):
+            ref = case.oracle_velocity(b)
+            errs = [rel_err(v[b, k], ref[k]) for k in range(w.n_chunks)]
+            print("fp32_rows stream", b, "P =", case.lens[b], "max rel err", max(errs))
+            assert max(errs) < tol(w), (b, errs)
+        case.ex.set_noise_state(9, 1)
+        pre = host(case.xd).copy()
+        case.ex.decode_step(case.xd, case.td, case.out)
+        post, out = host(case.xd), host(case.out)
+        mism = 0
+        for b in range(w.batch):
+            z = oracle.gaussian_chunk(9 + b, 1, w.chunk_len, w.action_dim)
+            new, ref_out = oracle.euler_emit_shift(pre[b], case.t[b], v[b], z, np.float32)
+            assert np.array_equal(out[b], ref_out), b
+            assert np.array_equal(post[b, :-1], new[:-1]), b
+            mism += int(np.count_nonzero(post[b, -1] != z))
+            assert np.max(np.abs(post[b, -1] - z)) <= 1e-6
+        assert mism <= 2
+    finally:
+        case.close()
+
+
 def test_causality_bit_exact_on_gpu():
     """Perturbing chunks after k leaves the velocity of chunks <= k unchanged, bitwise."""
     w = synth.workload("small_bf16")
