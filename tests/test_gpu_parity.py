@@ -62,6 +62,28 @@ def test_velocity_parity_small(name):
         case.close()
 
 
+@pytest.mark.parametrize("name,dh,gated", [("small_bf16", 192, False), ("small_bf16", 192, True),
+                                           ("small_fp32_b2", 64, False)])
+def test_velocity_parity_head_dim_and_plain_mlp(name, dh, gated):
+    """Head dim 192 (the register-staged bf16 attention) and the plain
+    tanh-GELU MLP (the GELU GEMM epilogue) against the oracle."""
+    base = synth.workload(name)
+    w = base.replace(name=f"{name}_dh{dh}_{'glu' if gated else 'mlp'}", head_dim=dh,
+                     n_q_heads=2 if dh == 192 else base.n_q_heads,
+                     n_kv_heads=1 if dh == 192 else base.n_kv_heads, mlp_gated=gated)
+    case = Case(w)
+    try:
+        v = case.gpu_velocity()
+        errs = []
+        for b in range(w.batch):
+            ref = case.oracle_velocity(b)
+            errs += [rel_err(v[b, k], ref[k]) for k in range(w.n_chunks)]
+        print(w.name, "max rel err", max(errs))
+        assert max(errs) < tol(w), errs
+    finally:
+        case.close()
+
+
 @pytest.mark.parametrize("name,lens", [("small_bf16_b3", [0, 1, 90]),
                                        ("small_fp32_b2", [0, 40])])
 def test_velocity_parity_edge_prefix_lengths(name, lens):

@@ -205,7 +205,8 @@ def test_p7_zero_modulation_makes_every_block_the_identity():
 def _textbook_prenorm_transformer(x, W, k_pre, v_pre, P, w):
     """Standard pre-norm transformer written token by token: weightless
     RMSNorm, rotary multi-query attention under the chunk-causal mask with
-    the prefix, GeGLU MLP, plain residuals, and an output head."""
+    the prefix, GeGLU MLP (w.mlp_gated) or a two-layer tanh-GELU MLP, plain
+    residuals, and an output head."""
     K, C, A = x.shape
     T, Hq, Hkv, dh = K * C, w.n_q_heads, w.n_kv_heads, w.head_dim
     rms = lambda r: r / math.sqrt(float(np.dot(r, r)) / r.size + w.rms_eps)
@@ -246,20 +247,25 @@ def _textbook_prenorm_transformer(x, W, k_pre, v_pre, P, w):
         hs = new
         for i in range(T):
             u2 = rms(hs[i])
-            hs[i] = hs[i] + (gelu(u2 @ W["wg"][l]) * (u2 @ W["wu"][l])) @ W["wd"][l]
+            if w.mlp_gated:
+                hs[i] = hs[i] + (gelu(u2 @ W["wg"][l]) * (u2 @ W["wu"][l])) @ W["wd"][l]
+            else:
+                hs[i] = hs[i] + gelu(u2 @ W["wu"][l]) @ W["wd"][l]
     return np.stack([rms(hs[i]) @ W["w_out"] + W["b_out"] for i in range(T)]).reshape(K, C, A)
 
 
-def test_p8_unit_gates_reduce_to_textbook_prenorm_transformer():
-    W, k, v, lens, x, t = _inputs(PIN)
-    Wd = PIN.width
+@pytest.mark.parametrize("gated", [True, False])
+def test_p8_unit_gates_reduce_to_textbook_prenorm_transformer(gated):
+    w = PIN.replace(mlp_gated=gated)
+    W, k, v, lens, x, t = _inputs(w)
+    Wd = w.width
     W["w_mod"] = [np.zeros_like(a) for a in W["w_mod"]]
     W["b_mod"] = [np.concatenate([np.zeros(2 * Wd), np.ones(Wd)]).astype(np.float32)
                   for _ in W["b_mod"]]
-    got = _v(PIN, W, k, v, lens, x, t)
+    got = _v(w, W, k, v, lens, x, t)
     P = int(lens[0])
     expect = _textbook_prenorm_transformer(x[0], W, k[:, 0].astype(np.float64),
-                                           v[:, 0].astype(np.float64), P, PIN)
+                                           v[:, 0].astype(np.float64), P, w)
     np.testing.assert_allclose(got, expect, rtol=0, atol=1e-11)
 
 
