@@ -63,10 +63,14 @@ def test_velocity_parity_small(name):
 
 
 @pytest.mark.parametrize("name,dh,gated", [("small_bf16", 192, False), ("small_bf16", 192, True),
-                                           ("small_fp32_b2", 64, False)])
+                                           ("small_fp32_b2", 64, False),
+                                           ("small_fp32_b2", 128, True),
+                                           ("small_fp32_b2", 192, True),
+                                           ("small_fp32_b2", 256, True)])
 def test_velocity_parity_head_dim_and_plain_mlp(name, dh, gated):
-    """Head dim 192 (the register-staged bf16 attention) and the plain
-    tanh-GELU MLP (the GELU GEMM epilogue) against the oracle."""
+    """Head dims 128-256 (bf16 192: the register-staged attention; fp32:
+    every instance of its attention kernel) and the plain tanh-GELU MLP (the
+    GELU GEMM epilogue) against the oracle."""
     base = synth.workload(name)
     w = base.replace(name=f"{name}_dh{dh}_{'glu' if gated else 'mlp'}", head_dim=dh,
                      n_q_heads=2 if dh == 192 else base.n_q_heads,
@@ -80,6 +84,37 @@ def test_velocity_parity_head_dim_and_plain_mlp(name, dh, gated):
             errs += [rel_err(v[b, k], ref[k]) for k in range(w.n_chunks)]
         print(w.name, "max rel err", max(errs))
         assert max(errs) < tol(w), errs
+    finally:
+        case.close()
+
+
+@pytest.mark.parametrize("name", ["small_bf16", "small_fp32_b2"])
+def test_max_width(name):
+    """Width 2048, the largest accepted: two column groups per thread in the
+    embedding and the split-K reduction, the generic velocity head and the
+    separate queue update (the fused head takes widths up to 1024).
+    Velocities against the oracle; one decode step, buffer and emitted chunk
+    bit for bit against the fp32 queue update of the GPU's own velocity."""
+    w = synth.workload(name).replace(name=f"{name}_w2048", width=2048, n_layers=1)
+    case = Case(w, noise_seed=4)
+    try:
+        v = case.gpu_velocity()
+        errs = []
+        for b in range(w.batch):
+            ref = case.oracle_velocity(b)
+            errs += [rel_err(v[b, k], ref[k]) for k in range(w.n_chunks)]
+        print(w.name, "max rel err", max(errs))
+        assert max(errs) < tol(w), errs
+        case.ex.set_noise_state(4, 0)
+        pre = host(case.xd).copy()
+        case.ex.decode_step(case.xd, case.td, case.out)
+        post, out = host(case.xd), host(case.out)
+        for b in range(w.batch):
+            z = oracle.gaussian_chunk(4 + b, 0, w.chunk_len, w.action_dim)
+            new, ref_out = oracle.euler_emit_shift(pre[b], case.t[b], v[b], z, np.float32)
+            assert np.array_equal(out[b], ref_out), b
+            assert np.array_equal(post[b, :-1], new[:-1]), b
+            assert np.max(np.abs(post[b, -1] - z)) <= 1e-6
     finally:
         case.close()
 
