@@ -4,6 +4,7 @@ checked here without a GPU."""
 import ctypes
 import os
 import re
+import subprocess
 
 import pytest
 
@@ -73,3 +74,21 @@ def test_invalid_config_rejected_before_device_work(field, value):
     st = fvb.lib().fv_create(ctypes.byref(hw.s), ctypes.byref(cfg), ctypes.byref(out))
     assert st == fvb.FV_ERR_INVALID_ARG
     assert out.value is None
+
+
+def test_header_is_plain_c99():
+    """The public header compiles as C99 on its own, pedantic, no warnings."""
+    r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror",
+                        "-fsyntax-only", "-x", "c", os.path.join(ROOT, "include", "flashvla.h")],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+
+
+def test_c_client_builds_and_links(tmp_path):
+    """A plain C99 program that drives the library compiles with gcc and links
+    against the built libflashvla.so (it runs in the GPU tests)."""
+    from tests.c_client.build import build_client
+    fvb.lib()  # the library is built
+    out = str(tmp_path / "decode_client")
+    build_client(out)
+    assert os.path.exists(out)
