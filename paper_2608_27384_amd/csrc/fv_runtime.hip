@@ -172,9 +172,6 @@ int attn_split(const Handle* h, int B) {
 // Output projection / down projection with the gated residual, fused with
 // the FiLM RMSNorm that feeds the next GEMM (norm_off < 0: none).
 // Kernels ahead of a GEMM pull its weights into the memory-side cache.
-#ifndef FV_PREFETCH
-#define FV_PREFETCH 1
-#endif
 
 // per: the FiLM-row sharing flag the maps' readers take (film_row), or nullptr.
 template <typename T>
@@ -189,7 +186,7 @@ void resid_block(Handle* h, const float* mod, const int* per, const T* A, const 
   if (ks > 1) {
     launch_resid_norm<T>(h->gw.ws, bf16_parts, ks, h->hres, mod, h->Nmod, gate_off, norm_off,
                          h->C, h->cfg.rms_eps, (T*)h->u, rowsT, W,
-                         FV_PREFETCH ? next_w : nullptr, next_bytes, s, per);
+                         next_w, next_bytes, s, per);
   } else {
     if (norm_off >= 0)
       launch_adarms<T>(h->hres, mod, h->Nmod, norm_off, h->C, h->cfg.rms_eps, (T*)h->u, rowsT,
@@ -235,7 +232,7 @@ AttnArgs attn_args(const Handle* h, const void* kar, const void* var, int B, int
                    const void* pf = nullptr, size_t pf_bytes = 0) {
   return AttnArgs{h->q,  kar,      var,  h->d_len, h->o,          h->part_o,
                   h->part_ml, B,   h->T, h->C,     h->Hq,         h->Hkv,
-                  h->dh, h->S,     n_split, h->d_valid, h->mask_mode, FV_PREFETCH ? pf : nullptr,
+                  h->dh, h->S,     n_split, h->d_valid, h->mask_mode, pf,
                   pf_bytes, h->d_len + h->Bmax};
 }
 
@@ -325,7 +322,7 @@ void proj_norm_only(Handle* h, int K, int gate_off, int norm_off, int rowsT, hip
   if (p.ks > 1)
     launch_resid_norm<T>(h->gw.ws, gemm_partials_bf16(p, h->bf16), p.ks, h->hres, h->mod, h->Nmod,
                          gate_off, norm_off, h->C, h->cfg.rms_eps, (T*)h->u, rowsT, h->W,
-                         FV_PREFETCH ? pf : nullptr, pf_bytes, s, h->film_per);
+                         pf, pf_bytes, s, h->film_per);
   else if (norm_off >= 0)
     launch_adarms<T>(h->hres, h->mod, h->Nmod, norm_off, h->C, h->cfg.rms_eps, (T*)h->u, rowsT,
                      h->W, s, h->film_per);
