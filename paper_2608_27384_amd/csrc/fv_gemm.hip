@@ -1086,13 +1086,13 @@ void launch_dma(const bf16_t* A, const bf16_t* Bt, int M, int N, int K, const Ge
 
 // Launches tile p.tile with the direct-to-LDS kernel when it has one;
 // returns false otherwise.  The 128x128 tile takes three stages when the
-// grid is about one round of the chip (the deeper ring hides load latency,
-// measured 1568 against 1864 us per batch-1 step with two), two stages when
-// it is many rounds (two workgroups then fit per CU and overlap each other).
+// grid fits the chip with one workgroup per CU (the deeper ring hides load
+// latency, measured 1568 against 1864 us per batch-1 step with two), two
+// stages otherwise (two workgroups then fit per CU and overlap each other).
 template <class Epi>
 bool try_dma(const bf16_t* A, const bf16_t* Bt, int M, int N, int K, const GemmPlan& p,
              const GemmWork& w, const Epi& epi, hipStream_t s) {
-  const bool rounds = (long)p.tiles * p.ks >= 512;
+  const bool rounds = (long)p.tiles * p.ks > 256;
   switch (p.tile) {
     case T256x256big: launch_dma<256, 256, 8, 2, 2>(A, Bt, M, N, K, p, w, epi, s); return true;
     case T128x128w8:
@@ -1127,32 +1127,39 @@ void run_gemm(const T* A, const T* Bt, int M, int N, int K, const GemmWork& w, c
 
 }  // namespace
 
-// Tile by row count: large M takes big tiles (fewer re-reads of A and W);
-// medium M takes 128x128 tiles when that still gives about 200 blocks, else
-// 64x128; small M takes 64- or 32-row tiles.  When fewer than 128 tiles
-// exist, k is split (KS a power of two, at least 4 k-tiles per split, at most
-// about 320 blocks) so that every CU streams its share of the weights.
-GemmPlan plan_gemm(int M, int N, int K, bool bf16) {
+// Tile by row count: large M takes 256x256 tiles (fewer re-reads of A and
+// W) when that still gives about 200 blocks, else 128x128 (bf16; two
+// workgroups per CU); medium M takes 128x128 tiles when that still gives
+// about 200 blocks, else 64x128; small M takes 64- or 32-row tiles.  When a
+// grid has fewer than 128 tiles, k is split (KS a power of two, at least 4
+// k-tiles per split, at most about 320 blocks) so that every CU streams its
+// share of the weights; with `reduce_fused` (the output and down
+// projections, whose split sum is fused into the next kernel at no extra
+// launch) grids of up to 160 tiles are split too.
+GemmPlan plan_gemm(int M, int N, int K, bool bf16, bool reduce_fused) {
   GemmPlan p;
   if (N % 128 || M <= 0) return p;
   const int bk = bf16 ? 64 : 32, nk = K / bk;
   auto ntiles = [&](int t) { return ((M + kTileBM[t] - 1) / kTileBM[t]) * (N / kTileBN[t]); };
-  if (M >= 4096)
-    p.tile = bf16 && N % 256 == 0 ? T256x256big : T256x128w8;
-  else if (M > 256)
+  if (M >= 4096) {
+    if (!bf16)
+      p.tile = T256x128w8;
+    else if (N % 256 == 0 && ntiles(T256x256big) >= 200)
+      p.tile = T256x256big;
+    else
+      p.tile = N % 256 == 0 ? T128x128w8 : T256x128w8;
+  } else if (M > 256) {
     p.tile = ntiles(T128x128w8) >= 200 ? T128x128w8 : T64x128w4;
-  else if (M > 32)
+  } else if (M > 32) {
     p.tile = T64x128w4;
-  else
+  } else {
     p.tile = T32x128w2;
-  const int bm = kTileBM[p.tile], bn = kTileBN[p.tile];
+  }
   p.tiles = ntiles(p.tile);
   p.ks = 1;
-  if (p.tiles < 128 && p.tile != T256x256big)
+  if ((p.tiles < 128 || (reduce_fused && p.tiles <= 160)) && p.tile != T256x256big)
     while ((long)p.tiles * p.ks * 2 <= 320 && nk / (p.ks * 2) >= 4 && p.ks < 8) p.ks *= 2;
   p.ws_floats = p.ks > 1 ? (size_t)p.ks * M * N : 0;
-  (void)bm;
-  (void)bn;
   return p;
 }
 
@@ -1166,7 +1173,7 @@ bool gemm_partials_bf16(const GemmPlan& p, bool bf16) {
 template <typename T>
 int gemm_partials(const T* A, const T* Bt, int M, int N, int K, const GemmWork& w,
                   hipStream_t s, bool* bf16_parts) {
-  const GemmPlan p = plan_gemm(M, N, K, sizeof(T) == 2);
+  const GemmPlan p = plan_gemm(M, N, K, sizeof(T) == 2, true);
   *bf16_parts = false;
   if (p.ks <= 1) return 1;
   if constexpr (sizeof(T) == 2) {

@@ -159,7 +159,9 @@ struct GemmPlan {
   int tile = -1, ks = 1, tiles = 0;  // tile shape id, split-K factor, output tiles
   size_t ws_floats = 0;              // split-K workspace this GEMM needs
 };
-GemmPlan plan_gemm(int M, int N, int K, bool bf16);
+// reduce_fused: the plan of an output or down projection (its split sum
+// runs inside the next kernel, so splitting costs no launch).
+GemmPlan plan_gemm(int M, int N, int K, bool bf16, bool reduce_fused = false);
 
 // Split-K scratch shared by every GEMM of a handle (launches are stream
 // ordered): partial tiles, fp32, or bf16 for the direct-to-LDS kernel with

@@ -318,7 +318,7 @@ void proj_gemm_only(Handle* h, const T* A, const T* Bt, int K, int gate_off, int
 template <typename T>
 void proj_norm_only(Handle* h, int K, int gate_off, int norm_off, int rowsT, hipStream_t s,
                     const void* pf, size_t pf_bytes) {
-  const GemmPlan p = plan_gemm(rowsT, h->W, K, h->bf16);
+  const GemmPlan p = plan_gemm(rowsT, h->W, K, h->bf16, true);
   if (p.ks > 1)
     launch_resid_norm<T>(h->gw.ws, gemm_partials_bf16(p, h->bf16), p.ks, h->hres, h->mod, h->Nmod,
                          gate_off, norm_off, h->C, h->cfg.rms_eps, (T*)h->u, rowsT, h->W,
@@ -551,8 +551,8 @@ StepScratch step_scratch(const Handle* h, int B) {
   }
   const int W = h->W, rk = B * h->K, rt = B * h->T, qd = h->Hq * h->dh;
   const GemmPlan ps[] = {plan_gemm(rk, W, W, h->bf16), plan_gemm(rk, h->Nmod, W, h->bf16),
-                         plan_gemm(rt, h->Nqkv, W, h->bf16), plan_gemm(rt, W, qd, h->bf16),
-                         plan_gemm(rt, h->Ngu, W, h->bf16), plan_gemm(rt, W, h->F, h->bf16)};
+                         plan_gemm(rt, h->Nqkv, W, h->bf16), plan_gemm(rt, W, qd, h->bf16, true),
+                         plan_gemm(rt, h->Ngu, W, h->bf16), plan_gemm(rt, W, h->F, h->bf16, true)};
   for (const GemmPlan& p : ps) r.ws = std::max(r.ws, round256(p.ws_floats * 4));
   return r;
 }
@@ -840,8 +840,8 @@ fv_status fv_create(const fv_weights* w, const fv_cfg* cfg, fv_handle* out) {
       for (int B = 1; B <= H.Bmax; ++B) {
         const int rk = B * H.K, rt = B * H.T;
         const GemmPlan ps[] = {plan_gemm(rk, W, W, b16), plan_gemm(rk, H.Nmod, W, b16),
-                               plan_gemm(rt, H.Nqkv, W, b16), plan_gemm(rt, W, qd, b16),
-                               plan_gemm(rt, H.Ngu, W, b16), plan_gemm(rt, W, F, b16)};
+                               plan_gemm(rt, H.Nqkv, W, b16), plan_gemm(rt, W, qd, b16, true),
+                               plan_gemm(rt, H.Ngu, W, b16), plan_gemm(rt, W, F, b16, true)};
         for (const GemmPlan& p : ps) ws = std::max(ws, p.ws_floats);
       }
       H.gw.ws = static_cast<float*>(dalloc(h, ws * 4));
@@ -1281,7 +1281,7 @@ fv_status fv_query(fv_handle h, int32_t what, int32_t batch, int64_t* value) {
         break;
       case FV_QUERY_OUT_PROJ_SPLITS:
         if (batch < 1 || batch > h->Bmax) fail(FV_ERR_INVALID_ARG, "batch outside 1..max_batch");
-        *value = plan_gemm(batch * h->T, h->W, h->Hq * h->dh, h->bf16).ks;
+        *value = plan_gemm(batch * h->T, h->W, h->Hq * h->dh, h->bf16, true).ks;
         break;
       case FV_QUERY_NOALLOC_SCRATCH_BYTES:
         if (batch < 1 || batch > h->Bmax) fail(FV_ERR_INVALID_ARG, "batch outside 1..max_batch");

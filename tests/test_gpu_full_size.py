@@ -116,6 +116,28 @@ def test_velocity_parity_ragged_large_m():
         case.close()
 
 
+@pytest.mark.parametrize("B", [2, 12])
+def test_velocity_parity_mid_batches(B):
+    """Batch sizes between the benchmarked ones take other GEMM plans: at
+    2 streams (1000 rows) the output and down projections split k in two;
+    at 12 (6000 rows) they run on 128 x 128 tiles, two workgroups per CU,
+    where 256 x 256 tiles would leave most CUs idle.  The first and last
+    streams against the oracle."""
+    w = synth.workload("batched64").replace(name=f"batched{B}", batch=B)
+    case = Case(w)
+    try:
+        assert case.ex.out_proj_splits() == (2 if B == 2 else 1)
+        v = case.gpu_velocity()
+        assert np.all(np.isfinite(v))
+        for b in (0, B - 1):
+            ref = case.oracle_velocity(b)
+            errs = [rel_err(v[b, k], ref[k]) for k in range(w.n_chunks)]
+            _say(f"batched{B} stream {b} (P={case.lens[b]}): max rel err {max(errs):.2e}")
+            assert max(errs) < tol(w), (b, errs)
+    finally:
+        case.close()
+
+
 def test_velocity_parity_many_short_streams():
     """90 streams of 50 tokens: 4500 rows take the 256-row GEMM tiles, whose
     128-row wave slabs span three or four streams, so the QKV epilogue looks
