@@ -1128,8 +1128,8 @@ void run_gemm(const T* A, const T* Bt, int M, int N, int K, const GemmWork& w, c
 }  // namespace
 
 // Tile by row count: large M takes 256x256 tiles (fewer re-reads of A and
-// W) when that still gives about 200 blocks, else 128x128 (bf16; two
-// workgroups per CU); medium M takes 128x128 tiles when that still gives
+// W) when that still gives about 200 blocks and no mostly idle second round,
+// else 128x128 (bf16; two workgroups per CU); medium M takes 128x128 tiles when that still gives
 // about 200 blocks (96 for an output or down projection), else 64x128;
 // small M takes 64- or 32-row tiles.  When a
 // grid has fewer than 128 tiles, k is split (KS a power of two, at least 4
@@ -1143,9 +1143,17 @@ GemmPlan plan_gemm(int M, int N, int K, bool bf16, bool reduce_fused) {
   const int bk = bf16 ? 64 : 32, nk = K / bk;
   auto ntiles = [&](int t) { return ((M + kTileBM[t] - 1) / kTileBM[t]) * (N / kTileBN[t]); };
   if (M >= 4096) {
+    // 256x256 tiles run one workgroup per CU, 128x128 tiles two.  A grid of
+    // two rounds of 256x256 tiles whose second round is mostly idle (under 72
+    // of 256 tiles) takes 128x128 tiles instead: measured per step, batch 16
+    // (QKV, 64 tiles in round two) 7.82 -> 7.67 ms, batch 36 (output and
+    // down projections, 28) 17.67 -> 17.00, batch 40 (60) 19.03 -> 18.73;
+    // slower at batch 44 (88) and 48 (120)
+    const long n256 = ntiles(T256x256big);
+    const bool big = n256 >= 200 && !(n256 > 256 && n256 <= 512 && n256 % 256 < 72);
     if (!bf16)
       p.tile = T256x128w8;
-    else if (N % 256 == 0 && ntiles(T256x256big) >= 200)
+    else if (N % 256 == 0 && big)
       p.tile = T256x256big;
     else
       p.tile = N % 256 == 0 ? T128x128w8 : T256x128w8;

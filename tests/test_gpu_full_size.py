@@ -116,14 +116,16 @@ def test_velocity_parity_ragged_large_m():
         case.close()
 
 
-@pytest.mark.parametrize("B", [2, 4, 12])
+@pytest.mark.parametrize("B", [2, 4, 12, 16, 36])
 def test_velocity_parity_mid_batches(B):
     """Batch sizes between the benchmarked ones take other GEMM plans: at
     2 streams (1000 rows) the output and down projections split k in two on
     64 x 128 tiles, at 4 (2000 rows) on 128 x 128 tiles; at 12 (6000 rows)
     they run unsplit on 128 x 128 tiles, two workgroups per CU, where
-    256 x 256 tiles would leave most CUs idle.  The first and last streams
-    against the oracle."""
+    256 x 256 tiles would leave most CUs idle; at 16 the QKV GEMM and at 36
+    the output and down projections take 128 x 128 tiles where 256 x 256
+    tiles would leave a second round mostly idle.  The first and last
+    streams against the oracle."""
     w = synth.workload("batched64").replace(name=f"batched{B}", batch=B)
     case = Case(w)
     try:
