@@ -119,6 +119,37 @@ def test_max_width(name):
         case.close()
 
 
+@pytest.mark.parametrize("name", ["tiny_fp32", "small_bf16"])
+def test_max_token_limits(name):
+    """The largest buffer and arena the handle accepts: K = 256 chunks of 16
+    actions (K * C = 4096 query rows) after a 28672-token prefix, so the arena
+    holds max_prefix + K * C = 32768 rows and the last chunk attends to all of
+    them.  Velocities of every chunk against the oracle; one decode step,
+    buffer and emitted chunk bit for bit against the fp32 queue update of the
+    GPU's own velocity."""
+    w = synth.workload(name).replace(name=f"{name}_maxtok", n_layers=1, n_chunks=256,
+                                     chunk_len=16, prefix_len=28672, batch=1)
+    assert w.tokens == 4096 and w.max_prefix + w.tokens == 32768
+    case = Case(w, noise_seed=6)
+    try:
+        v = case.gpu_velocity()
+        ref = case.oracle_velocity(0)
+        errs = [rel_err(v[0, k], ref[k]) for k in range(w.n_chunks)]
+        print(w.name, "max rel err", max(errs), "at chunk", int(np.argmax(errs)))
+        assert max(errs) < tol(w), errs
+        case.ex.set_noise_state(6, 0)
+        pre = host(case.xd).copy()
+        case.ex.decode_step(case.xd, case.td, case.out)
+        post, out = host(case.xd), host(case.out)
+        z = oracle.gaussian_chunk(6, 0, w.chunk_len, w.action_dim)
+        new, ref_out = oracle.euler_emit_shift(pre[0], case.t[0], v[0], z, np.float32)
+        assert np.array_equal(out[0], ref_out)
+        assert np.array_equal(post[0, :-1], new[:-1])
+        assert np.max(np.abs(post[0, -1] - z)) <= 1e-6
+    finally:
+        case.close()
+
+
 @pytest.mark.parametrize("name,lens", [("small_bf16_b3", [0, 1, 90]),
                                        ("small_fp32_b2", [0, 40])])
 def test_velocity_parity_edge_prefix_lengths(name, lens):
