@@ -150,6 +150,45 @@ def test_max_token_limits(name):
         case.close()
 
 
+@pytest.mark.parametrize("name,plen", [("tiny_fp32", (0, 64)), ("small_bf16", (0, 70))])
+def test_max_batch(name, plen):
+    """4096 streams, the largest batch a handle accepts, with ragged prefixes
+    (some empty).  The oracle runs on a seeded sample of streams (both ends
+    and six inside); every stream's output must be finite; one decode step
+    then matches the fp32 queue update of the GPU's own velocity bit for bit
+    on every stream, and the refill matches the oracle's Philox draw on the
+    sampled ones."""
+    w = synth.workload(name).replace(name=f"{name}_b4096", n_layers=1, batch=4096,
+                                     prefix_len=plen)
+    case = Case(w, noise_seed=8)
+    try:
+        assert int(case.lens.min()) == 0
+        v = case.gpu_velocity()
+        assert np.isfinite(v).all()
+        rng = np.random.default_rng(4096)
+        sample = sorted({0, 1, w.batch - 1, *rng.integers(2, w.batch - 1, size=5).tolist()})
+        errs = []
+        for b in sample:
+            ref = case.oracle_velocity(b)
+            errs += [rel_err(v[b, k], ref[k]) for k in range(w.n_chunks)]
+        print(w.name, "streams", sample, "max rel err", max(errs))
+        assert max(errs) < tol(w), errs
+        case.ex.set_noise_state(8, 0)
+        pre = host(case.xd).copy()
+        case.ex.decode_step(case.xd, case.td, case.out)
+        post, out = host(case.xd), host(case.out)
+        zero = np.zeros((w.chunk_len, w.action_dim), np.float32)
+        for b in range(w.batch):
+            new, ref_out = oracle.euler_emit_shift(pre[b], case.t[b], v[b], zero, np.float32)
+            assert np.array_equal(out[b], ref_out), b
+            assert np.array_equal(post[b, :-1], new[:-1]), b
+        for b in sample:
+            z = oracle.gaussian_chunk(8 + b, 0, w.chunk_len, w.action_dim)
+            assert np.max(np.abs(post[b, -1] - z)) <= 1e-6, b
+    finally:
+        case.close()
+
+
 @pytest.mark.parametrize("name,lens", [("small_bf16_b3", [0, 1, 90]),
                                        ("small_fp32_b2", [0, 40])])
 def test_velocity_parity_edge_prefix_lengths(name, lens):
